@@ -1,0 +1,186 @@
+/*
+ * lazy_attn.h - C ABI of the LazyAttention hot path for AMD Instinct MI355X (gfx950).
+ *
+ * LazyAttention (arXiv 2606.04302) keeps the KV cache free of positional encoding and applies RoPE inside the
+ * attention kernel, at the position each retrieved chunk takes in the current request (Sec. 3.1 "Deferred
+ * encoding"; Sec. 3.2 "Efficient Rotation with Tiling").  One stored copy of a chunk can therefore serve any number
+ * of requests at different offsets, in the same batch, without writing a re-rotated copy (problem statement at the
+ * start of Sec. 3).
+ *
+ * Conventions shared by every entry point
+ *  - All tensors live in device memory and are owned by the caller.  The library allocates no device memory,
+ *    never synchronises the device, and enqueues all work asynchronously on `stream` (a hipStream_t; NULL = the
+ *    null stream).  Inputs are read-only; in particular the chunk store is never written, so concurrent requests
+ *    that share a chunk cannot race (Sec. 1: in-place re-encoding races when two prompts share data).
+ *  - Element type of q, k, v and out is bfloat16 (raw 16-bit storage, passed as void*); accumulation is fp32.
+ *  - head_dim D is 64 or 128.  RoPE pairs dimension t with t + D/2 (half-split, the K1/K2 halves of Sec. 3.2
+ *    "Prefilling"): x1' = x1 cos(p theta_t) - x2 sin(p theta_t), x2' = x1 sin(p theta_t) + x2 cos(p theta_t),
+ *    theta_t = rope_base^(-2t/D) unless params->inv_freq supplies the D/2 frequencies (RoPE variants, Sec. 3.5).
+ *  - GQA: query head h reads KV head h / (num_q_heads / num_kv_heads) (Sec. 3.5).
+ *  - Causal rule: a key at position pk is visible to a query at position pq iff pk <= pq (positions, not table
+ *    indices, decide, so chunks may sit at arbitrary offsets).  A query that sees no key yields out = 0 and
+ *    lse = -inf.
+ *  - Return value: LAZY_OK (0) on success, a negative LAZY_E* code otherwise.  Scalar arguments are checked on
+ *    every call; the contents of device tables are only checked by lazy_attn_validate (host copies).  Errors
+ *    never cross the ABI as exceptions.
+ */
+#ifndef LAZY_ATTN_H
+#define LAZY_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define LAZY_API __attribute__((visibility("default")))
+#else
+#define LAZY_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LAZY_OK 0
+#define LAZY_EINVAL (-1)       /* bad scalar argument or null pointer */
+#define LAZY_EUNSUPPORTED (-2) /* valid request outside what the kernels implement (e.g. head_dim not 64/128) */
+#define LAZY_EWORKSPACE (-3)   /* workspace missing or smaller than the *_workspace_size query returned */
+#define LAZY_EHIP (-4)         /* the HIP runtime reported an error at launch */
+#define LAZY_EDATA (-5)        /* lazy_attn_validate: a table entry breaks the layout contract */
+
+/* Largest position (exclusive) a key or query may take. */
+#define LAZY_MAX_POS (1 << 24)
+
+/*
+ * One use of a stored chunk by one request (the paper's per-document offset, Sec. 3.2 "Prefilling": a single
+ * offset for the whole document).  The chunk's keys j = 0..len-1 take positions pos_offset + j in this request.
+ * Storage is position-free and head-major: key j of KV head g is the D contiguous elements at
+ *     k_pool + k_offset + (g * k_stride + j) * D
+ * and its value at v_pool + v_offset + (g * v_stride + j) * D (offsets and strides in elements / tokens; a
+ * stride is the chunk's capacity, >= len, so a growing decode tail can be appended in place).
+ * Requirements: len >= 1, pos_offset >= 0, pos_offset + len <= LAZY_MAX_POS, k_stride >= len, v_stride >= len,
+ * offsets >= 0 and multiples of 8 (16-byte alignment).  32 bytes, no padding.
+ */
+typedef struct lazy_chunk {
+  int64_t k_offset;
+  int64_t v_offset;
+  int32_t len;
+  int32_t pos_offset;
+  int32_t k_stride;
+  int32_t v_stride;
+} lazy_chunk_t;
+
+typedef struct lazy_attn_params {
+  int32_t num_q_heads;   /* Hq */
+  int32_t num_kv_heads;  /* Hkv, divides Hq */
+  int32_t head_dim;      /* D: 64 or 128 */
+  int32_t causal;        /* 1: position-based causal rule; 0: every key visible */
+  float rope_base;       /* theta_t = rope_base^(-2t/D); ignored if inv_freq != NULL */
+  float softmax_scale;   /* 0 => 1/sqrt(D) (Eqn. standard attention) */
+  const float* inv_freq; /* optional device array of D/2 fp32 frequencies theta_t (scaled / NTK tables) */
+  int32_t num_splits;    /* 0 => chosen by the library; otherwise the number of KV splits per request */
+  int32_t reserved;      /* must be 0 */
+} lazy_attn_params_t;
+
+/*
+ * Prefill (Sec. 3.2 "Prefilling"; Fig. 3(b)): every request's new query tokens attend over all keys of its chunk
+ * table, each key rotated inside the kernel at pos_offset + j, queries rotated at their own positions.
+ *   q            [total_q][Hq][D] bf16, NoPE queries; rows of request r are q_start[r] .. q_start[r+1]-1
+ *   q_start      [batch+1] int32 device, non-decreasing, q_start[0] = 0
+ *   q_pos0       [batch] int32 device: token i of request r sits at position q_pos0[r] + i
+ *   k_pool,v_pool bf16 device base pointers of the chunk store (may be the same pointer)
+ *   chunks       device array of lazy_chunk_t, all requests back to back; request r owns
+ *                chunks[chunk_start[r] .. chunk_start[r+1]-1].  The request's own new K/V (if it attends to
+ *                itself) is simply one of its records, usually the last, at pos_offset = q_pos0[r].
+ *   chunk_start  [batch+1] int32 device prefix sums
+ *   max_q_len    upper bound of any request's query count (sizes the grid)
+ *   max_kv_len   upper bound of any request's total key count (sizes the KV split)
+ *   out          [total_q][Hq][D] bf16, fully overwritten
+ *   lse          [total_q][Hq] fp32 natural-log sum-exp of the scaled scores, or NULL
+ *   workspace    device scratch of at least lazy_attn_prefill_workspace_size(...) bytes (may be NULL if 0)
+ */
+LAZY_API int lazy_attn_prefill(const lazy_attn_params_t* params, const void* q, const int32_t* q_start,
+                      const int32_t* q_pos0, const void* k_pool, const void* v_pool, const lazy_chunk_t* chunks,
+                      const int32_t* chunk_start, int32_t batch, int32_t total_q, int32_t max_q_len,
+                      int32_t max_kv_len, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
+LAZY_API size_t lazy_attn_prefill_workspace_size(const lazy_attn_params_t* params, int32_t batch, int32_t total_q,
+                                        int32_t max_q_len, int32_t max_kv_len);
+
+/*
+ * Decode (Sec. 3.2 "Decoding"; Fig. 3(c)): one new query token per request at q_pos[r] attends over its chunk
+ * table; the token's own K/V must already be appended to one of the request's chunks.  KV is split across
+ * workgroups (split-KV) and the partial softmax states are merged by lazy_attn_combine's kernel.
+ *   q [batch][Hq][D] bf16, q_pos [batch] int32 device, out [batch][Hq][D] bf16, lse [batch][Hq] fp32 or NULL.
+ *   Other arguments as for prefill.
+ */
+LAZY_API int lazy_attn_decode(const lazy_attn_params_t* params, const void* q, const int32_t* q_pos, const void* k_pool,
+                     const void* v_pool, const lazy_chunk_t* chunks, const int32_t* chunk_start, int32_t batch,
+                     int32_t max_kv_len, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
+LAZY_API size_t lazy_attn_decode_workspace_size(const lazy_attn_params_t* params, int32_t batch, int32_t max_kv_len);
+
+/*
+ * Split-KV merge (standard log-sum-exp combination of partial softmax states over disjoint key sets):
+ * with M = max_s m[s][row], w_s = exp(m[s][row] - M):
+ *     out[row] = sum_s w_s acc[s][row][:] / sum_s w_s l[s][row],   lse[row] = M + ln(sum_s w_s l[s][row]).
+ *   part_acc [splits][rows][D] fp32, part_ml [splits][rows][2] fp32 holding (m, l) with m the natural-log-domain
+ *   running max of the scaled scores (-inf for an empty split, then l = 0 and acc = 0).
+ *   out [rows][D] bf16; lse [rows] fp32 or NULL.  Rows whose every split is empty get out = 0, lse = -inf.
+ */
+LAZY_API int lazy_attn_combine(const float* part_acc, const float* part_ml, int32_t splits, int32_t rows, int32_t head_dim,
+                      void* out, float* lse, void* stream);
+
+/*
+ * Materialise-then-attend baseline, step 1 (the re-encoding copy that LazyAttention avoids; Block-Attention's
+ * rotate-and-copy path described in the appendix "Experiments Details"): for every record i of every request,
+ * write R(pos_offset + j) k_j into k_out, request after request, so that each request's rotated keys form one
+ * contiguous region: record i's block [Hkv][len_i][D] starts at element sum_{i' < i} Hkv * len_{i'} * D.
+ * chunks_out (device, same count) receives the records that describe the copy: k_offset into k_out,
+ * k_stride = len, v_offset / v_stride / len / pos_offset unchanged (values are read in place).
+ *   num_records = chunk_start[batch]; total_kv = sum of all len (k_out holds Hkv * total_kv * D elements).
+ */
+LAZY_API int lazy_materialize_k(const lazy_attn_params_t* params, const void* k_pool, const lazy_chunk_t* chunks,
+                       int32_t num_records, int32_t max_chunk_len, int64_t total_kv, void* k_out,
+                       lazy_chunk_t* chunks_out, void* stream);
+
+/*
+ * Materialise-then-attend baseline, step 2: ordinary attention over keys that already carry their positions
+ * (k_pool / chunks as produced by lazy_materialize_k); queries are still rotated at their positions.  Same
+ * arguments and workspace sizes as lazy_attn_prefill / lazy_attn_decode.
+ */
+LAZY_API int lazy_plain_attn_prefill(const lazy_attn_params_t* params, const void* q, const int32_t* q_start,
+                            const int32_t* q_pos0, const void* k_pool, const void* v_pool,
+                            const lazy_chunk_t* chunks, const int32_t* chunk_start, int32_t batch, int32_t total_q,
+                            int32_t max_q_len, int32_t max_kv_len, void* out, float* lse, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+LAZY_API int lazy_plain_attn_decode(const lazy_attn_params_t* params, const void* q, const int32_t* q_pos,
+                           const void* k_pool, const void* v_pool, const lazy_chunk_t* chunks,
+                           const int32_t* chunk_start, int32_t batch, int32_t max_kv_len, void* out, float* lse,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Host-side check of the table contents against the layout contract, on HOST copies of the tables (CPU only, no
+ * device access).  k_pool_elems / v_pool_elems are the pool sizes in elements.  Returns LAZY_OK or LAZY_EDATA and
+ * writes the offending record / request index and a reason to *bad_index / reason (either may be NULL).
+ * q_start / q_pos0 may be NULL to skip query checks (decode passes q_start = NULL and q_pos as q_pos0).
+ * Checks: prefix sums monotone and starting at 0; every record as required by lazy_chunk_t; K/V ranges inside
+ * the pools; positions below LAZY_MAX_POS; with the causal rule, every query sees at least one key.
+ */
+LAZY_API int lazy_attn_validate(const lazy_attn_params_t* params, const int32_t* q_start, const int32_t* q_pos0,
+                       const lazy_chunk_t* chunks, const int32_t* chunk_start, int32_t batch, int64_t k_pool_elems,
+                       int64_t v_pool_elems, int64_t* bad_index, const char** reason);
+
+/* Static text for a LAZY_* code. */
+LAZY_API const char* lazy_attn_strerror(int code);
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+LAZY_API int lazy_attn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LAZY_ATTN_H */

@@ -1,0 +1,247 @@
+// C ABI of the LazyAttention hot path: argument checks, launch configuration and dispatch to the HIP kernels.
+// The library never allocates device memory and never synchronises; every launch goes to the caller's stream.
+#include <hip/hip_runtime_api.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "lazy_attn.h"
+#include "lazy_attn_internal.h"
+
+namespace {
+
+constexpr int kTargetWorkgroups = 1024;  // 256 CUs x ~4 resident workgroups
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int check_params(const lazy_attn_params_t* p) {
+  if (!p) return LAZY_EINVAL;
+  if (p->num_q_heads <= 0 || p->num_kv_heads <= 0 || p->num_q_heads % p->num_kv_heads != 0) return LAZY_EINVAL;
+  if (p->causal != 0 && p->causal != 1) return LAZY_EINVAL;
+  if (!isfinite(p->softmax_scale) || p->softmax_scale < 0.f) return LAZY_EINVAL;
+  if (!p->inv_freq && !(isfinite(p->rope_base) && p->rope_base > 0.f)) return LAZY_EINVAL;
+  if (p->num_splits < 0 || p->reserved != 0) return LAZY_EINVAL;
+  if (p->head_dim != 64 && p->head_dim != 128) return LAZY_EUNSUPPORTED;
+  return LAZY_OK;
+}
+
+float scale_log2(const lazy_attn_params_t* p) {
+  const float s = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / sqrtf((float)p->head_dim);
+  return s * 1.4426950408889634f;
+}
+
+int prefill_q_tiles(const lazy_attn_params_t* p, int32_t max_q_len) {
+  const int64_t g = p->num_q_heads / p->num_kv_heads;
+  return (int)ceil_div((int64_t)max_q_len * g, lazy::kPrefillRows);
+}
+
+int prefill_splits(const lazy_attn_params_t* p, int32_t batch, int32_t max_q_len, int32_t max_kv_len) {
+  if (p->num_splits > 0) return p->num_splits;
+  const int64_t base = (int64_t)prefill_q_tiles(p, max_q_len) * p->num_kv_heads * batch;
+  const int64_t tiles = ceil_div(max_kv_len, lazy::kPrefillTileKeys);
+  int64_t s = base > 0 ? ceil_div(kTargetWorkgroups, base) : 1;
+  const int64_t cap = tiles / 4 > 1 ? tiles / 4 : 1;  // keep at least ~4 key tiles per split
+  if (s > cap) s = cap;
+  if (s > 64) s = 64;
+  return s < 1 ? 1 : (int)s;
+}
+
+int decode_head_groups(const lazy_attn_params_t* p) {
+  const int g = p->num_q_heads / p->num_kv_heads;
+  return (g + lazy::kDecodeHeadsPerGroup - 1) / lazy::kDecodeHeadsPerGroup;
+}
+
+int decode_splits(const lazy_attn_params_t* p, int32_t batch, int32_t max_kv_len) {
+  if (p->num_splits > 0) return p->num_splits;
+  const int64_t base = (int64_t)batch * p->num_kv_heads * decode_head_groups(p);
+  const int64_t tiles = ceil_div(max_kv_len, lazy::kDecodeTileKeys);
+  int64_t s = base > 0 ? ceil_div(2 * kTargetWorkgroups, base) : 1;
+  const int64_t cap = tiles / 2 > 1 ? tiles / 2 : 1;
+  if (s > cap) s = cap;
+  if (s > 64) s = 64;
+  return s < 1 ? 1 : (int)s;
+}
+
+size_t split_workspace(int splits, int64_t rows, int d) {
+  if (splits <= 1) return 0;
+  return (size_t)splits * (size_t)rows * (size_t)(d + 2) * sizeof(float);
+}
+
+int status(hipError_t e) { return e == hipSuccess ? LAZY_OK : LAZY_EHIP; }
+
+int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const int32_t* q_start,
+                const int32_t* q_pos0, const void* k_pool, const void* v_pool, const lazy_chunk_t* chunks,
+                const int32_t* chunk_start, int32_t batch, int32_t total_q, int32_t max_q_len, int32_t max_kv_len,
+                void* out, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  int e = check_params(p);
+  if (e != LAZY_OK) return e;
+  if (batch < 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0) return LAZY_EINVAL;
+  if (batch == 0 || total_q == 0) return LAZY_OK;
+  if (max_q_len == 0) return LAZY_EINVAL;
+  if (!q || !q_start || !q_pos0 || !k_pool || !v_pool || !chunks || !chunk_start || !out) return LAZY_EINVAL;
+  const int splits = prefill_splits(p, batch, max_q_len, max_kv_len);
+  const int q_tiles = prefill_q_tiles(p, max_q_len);
+  if ((int64_t)batch * splits > 65535 || p->num_kv_heads > 65535) return LAZY_EUNSUPPORTED;
+  const int64_t rows = (int64_t)total_q * p->num_q_heads;
+  const size_t need = split_workspace(splits, rows, p->head_dim);
+  if (need > 0 && (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 15u))) return LAZY_EWORKSPACE;
+
+  lazy::AttnArgs a = {};
+  a.q = static_cast<const uint16_t*>(q);
+  a.q_start = q_start;
+  a.q_pos0 = q_pos0;
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.chunks = chunks;
+  a.chunk_start = chunk_start;
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse;
+  a.ws_acc = need ? static_cast<float*>(workspace) : nullptr;
+  a.ws_ml = need ? static_cast<float*>(workspace) + (size_t)splits * rows * p->head_dim : nullptr;
+  a.inv_freq = p->inv_freq;
+  a.batch = batch;
+  a.total_q = total_q;
+  a.hq = p->num_q_heads;
+  a.hkv = p->num_kv_heads;
+  a.group = p->num_q_heads / p->num_kv_heads;
+  a.causal = p->causal;
+  a.splits = splits;
+  a.q_tiles = q_tiles;
+  a.head_groups = 1;
+  a.rope_base = p->rope_base;
+  a.scale_log2 = scale_log2(p);
+  return status(lazy::launch_prefill(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
+}
+
+int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const int32_t* q_pos, const void* k_pool,
+               const void* v_pool, const lazy_chunk_t* chunks, const int32_t* chunk_start, int32_t batch,
+               int32_t max_kv_len, void* out, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  int e = check_params(p);
+  if (e != LAZY_OK) return e;
+  if (batch < 0 || max_kv_len < 0) return LAZY_EINVAL;
+  if (batch == 0) return LAZY_OK;
+  if (!q || !q_pos || !k_pool || !v_pool || !chunks || !chunk_start || !out) return LAZY_EINVAL;
+  const int splits = decode_splits(p, batch, max_kv_len);
+  const int hg = decode_head_groups(p);
+  if (batch > 65535 || (int64_t)p->num_kv_heads * hg > 65535) return LAZY_EUNSUPPORTED;
+  const int64_t rows = (int64_t)batch * p->num_q_heads;
+  const size_t need = split_workspace(splits, rows, p->head_dim);
+  if (need > 0 && (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 15u))) return LAZY_EWORKSPACE;
+
+  lazy::AttnArgs a = {};
+  a.q = static_cast<const uint16_t*>(q);
+  a.q_start = nullptr;
+  a.q_pos0 = q_pos;
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.chunks = chunks;
+  a.chunk_start = chunk_start;
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse;
+  a.ws_acc = need ? static_cast<float*>(workspace) : nullptr;
+  a.ws_ml = need ? static_cast<float*>(workspace) + (size_t)splits * rows * p->head_dim : nullptr;
+  a.inv_freq = p->inv_freq;
+  a.batch = batch;
+  a.total_q = batch;
+  a.hq = p->num_q_heads;
+  a.hkv = p->num_kv_heads;
+  a.group = p->num_q_heads / p->num_kv_heads;
+  a.causal = p->causal;
+  a.splits = splits;
+  a.q_tiles = 1;
+  a.head_groups = hg;
+  a.rope_base = p->rope_base;
+  a.scale_log2 = scale_log2(p);
+  return status(lazy::launch_decode(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t lazy_attn_prefill_workspace_size(const lazy_attn_params_t* params, int32_t batch, int32_t total_q,
+                                        int32_t max_q_len, int32_t max_kv_len) {
+  if (check_params(params) != LAZY_OK || batch <= 0 || total_q <= 0 || max_q_len <= 0 || max_kv_len < 0) return 0;
+  const int splits = prefill_splits(params, batch, max_q_len, max_kv_len);
+  return split_workspace(splits, (int64_t)total_q * params->num_q_heads, params->head_dim);
+}
+
+size_t lazy_attn_decode_workspace_size(const lazy_attn_params_t* params, int32_t batch, int32_t max_kv_len) {
+  if (check_params(params) != LAZY_OK || batch <= 0 || max_kv_len < 0) return 0;
+  const int splits = decode_splits(params, batch, max_kv_len);
+  return split_workspace(splits, (int64_t)batch * params->num_q_heads, params->head_dim);
+}
+
+int lazy_attn_prefill(const lazy_attn_params_t* params, const void* q, const int32_t* q_start,
+                      const int32_t* q_pos0, const void* k_pool, const void* v_pool, const lazy_chunk_t* chunks,
+                      const int32_t* chunk_start, int32_t batch, int32_t total_q, int32_t max_q_len,
+                      int32_t max_kv_len, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  return run_prefill(true, params, q, q_start, q_pos0, k_pool, v_pool, chunks, chunk_start, batch, total_q,
+                     max_q_len, max_kv_len, out, lse, workspace, workspace_bytes, stream);
+}
+
+int lazy_plain_attn_prefill(const lazy_attn_params_t* params, const void* q, const int32_t* q_start,
+                            const int32_t* q_pos0, const void* k_pool, const void* v_pool,
+                            const lazy_chunk_t* chunks, const int32_t* chunk_start, int32_t batch, int32_t total_q,
+                            int32_t max_q_len, int32_t max_kv_len, void* out, float* lse, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  return run_prefill(false, params, q, q_start, q_pos0, k_pool, v_pool, chunks, chunk_start, batch, total_q,
+                     max_q_len, max_kv_len, out, lse, workspace, workspace_bytes, stream);
+}
+
+int lazy_attn_decode(const lazy_attn_params_t* params, const void* q, const int32_t* q_pos, const void* k_pool,
+                     const void* v_pool, const lazy_chunk_t* chunks, const int32_t* chunk_start, int32_t batch,
+                     int32_t max_kv_len, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  return run_decode(true, params, q, q_pos, k_pool, v_pool, chunks, chunk_start, batch, max_kv_len, out, lse,
+                    workspace, workspace_bytes, stream);
+}
+
+int lazy_plain_attn_decode(const lazy_attn_params_t* params, const void* q, const int32_t* q_pos,
+                           const void* k_pool, const void* v_pool, const lazy_chunk_t* chunks,
+                           const int32_t* chunk_start, int32_t batch, int32_t max_kv_len, void* out, float* lse,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  return run_decode(false, params, q, q_pos, k_pool, v_pool, chunks, chunk_start, batch, max_kv_len, out, lse,
+                    workspace, workspace_bytes, stream);
+}
+
+int lazy_attn_combine(const float* part_acc, const float* part_ml, int32_t splits, int32_t rows, int32_t head_dim,
+                      void* out, float* lse, void* stream) {
+  if (head_dim != 64 && head_dim != 128) return LAZY_EUNSUPPORTED;
+  if (splits <= 0 || rows < 0) return LAZY_EINVAL;
+  if (rows == 0) return LAZY_OK;
+  if (!part_acc || !part_ml || !out || ((uintptr_t)part_acc & 15u)) return LAZY_EINVAL;
+  return status(lazy::launch_combine(part_acc, part_ml, splits, rows, head_dim, static_cast<uint16_t*>(out), lse,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+int lazy_materialize_k(const lazy_attn_params_t* params, const void* k_pool, const lazy_chunk_t* chunks,
+                       int32_t num_records, int32_t max_chunk_len, int64_t total_kv, void* k_out,
+                       lazy_chunk_t* chunks_out, void* stream) {
+  int e = check_params(params);
+  if (e != LAZY_OK) return e;
+  if (num_records < 0 || max_chunk_len < 0 || total_kv < 0) return LAZY_EINVAL;
+  if (num_records == 0) return LAZY_OK;
+  if (!k_pool || !chunks || !chunks_out || (total_kv > 0 && !k_out)) return LAZY_EINVAL;
+  if (num_records > 65535 || params->num_kv_heads > 65535) return LAZY_EUNSUPPORTED;
+  return status(lazy::launch_materialize(static_cast<const uint16_t*>(k_pool), chunks, num_records, max_chunk_len,
+                                         params->num_kv_heads, params->head_dim, params->rope_base,
+                                         params->inv_freq, static_cast<uint16_t*>(k_out), chunks_out,
+                                         static_cast<hipStream_t>(stream)));
+}
+
+const char* lazy_attn_strerror(int code) {
+  switch (code) {
+    case LAZY_OK: return "success";
+    case LAZY_EINVAL: return "invalid argument";
+    case LAZY_EUNSUPPORTED: return "unsupported configuration";
+    case LAZY_EWORKSPACE: return "workspace missing, too small or misaligned";
+    case LAZY_EHIP: return "HIP runtime error at launch";
+    case LAZY_EDATA: return "chunk or query table violates the layout contract";
+    default: return "unknown error";
+  }
+}
+
+int lazy_attn_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,52 @@
+// Internal interface between the C ABI (lazy_attn_api.cpp) and the HIP kernels (lazy_attn_kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#include "lazy_attn.h"
+
+namespace lazy {
+
+// Everything one attention launch needs.  Pointers are device pointers.
+struct AttnArgs {
+  const uint16_t* q;          // [total_q][hq][D] bf16 bits
+  const int32_t* q_start;     // [batch+1]
+  const int32_t* q_pos0;      // [batch]
+  const uint16_t* k_pool;     // bf16 bits
+  const uint16_t* v_pool;
+  const lazy_chunk_t* chunks;
+  const int32_t* chunk_start; // [batch+1]
+  uint16_t* out;              // [total_q][hq][D] bf16 bits
+  float* lse;                 // [total_q][hq] or null
+  float* ws_acc;              // [splits][total_q*hq][D] fp32, null when splits == 1
+  float* ws_ml;               // [splits][total_q*hq][2] fp32 (m, l), null when splits == 1
+  const float* inv_freq;      // [D/2] or null
+  int32_t batch;
+  int32_t total_q;
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;              // hq / hkv
+  int32_t causal;
+  int32_t splits;
+  int32_t q_tiles;            // prefill: row tiles per (request, kv head)
+  int32_t head_groups;        // decode: ceil(group / 16)
+  float rope_base;
+  float scale_log2;           // softmax scale * log2(e)
+};
+
+// Packed rows (token, head in group) handled by one prefill workgroup, and keys per decode tile.
+constexpr int kPrefillRows = 128;
+constexpr int kPrefillTileKeys = 64;
+constexpr int kDecodeTileKeys = 128;
+constexpr int kDecodeHeadsPerGroup = 16;
+
+hipError_t launch_prefill(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t stream);
+hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t stream);
+hipError_t launch_combine(const float* acc, const float* ml, int splits, int rows, int head_dim, uint16_t* out,
+                          float* lse, hipStream_t stream);
+hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
+                              int max_chunk_len, int hkv, int head_dim, float rope_base, const float* inv_freq,
+                              uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t stream);
+
+}  // namespace lazy

@@ -1,0 +1,801 @@
+// HIP kernels of the LazyAttention hot path for gfx950 (MI355X / CDNA4).
+//
+// The chunk store holds K and V without positional encoding (Sec. 3.1 "Deferred encoding").  Every kernel that
+// reads K rotates it on the way from HBM into LDS, at position pos_offset + j of the chunk in the current request
+// (Sec. 3.2 "Prefilling": one rotation of the two half-dimensions per key, never "back to zero then forward").
+//
+// Data path of one key tile (64 keys per sub-tile, shared by the four waves of a workgroup):
+//   global K rows (bf16, natural layout) --16 B loads--> registers --fp32 rotation--> bf16 --> LDS K tile
+//   global V rows --16 B loads--> registers --4x8 transpose (v_perm)--> LDS V^T tile
+// The rotation is done once per workgroup and tile (not once per wave), which matters on gfx950 where the bf16
+// MFMA rate is 16x the fp32 VALU rate: the relative cost of rotating K is 3/(4M) in FLOPs (eq. prefilling) but
+// paid at VALU speed.
+//
+// Rotation angles are stateless (Appendix "Long-Context Scalability and Numerical Stability": absolute indices,
+// no recurrence).  theta_t is held in revolutions per position in fp64; for a tile whose row 0 sits at position b
+// the workgroup computes cos/sin(b theta_t) once per t, and each loader thread keeps cos/sin(delta theta_t) for
+// its fixed row delta in registers; the angle of row b + delta follows by one angle addition.
+//
+// Operand layouts (verified for v_mfma_f32_32x32x16_bf16 and v_mfma_f32_16x16x32_bf16):
+//   32x32x16: A[i][k] in lane i%32 ... k = 8*(lane/32)+e; B[k][j] in lane j%32, k = 8*(lane/32)+e;
+//             C[8*(r/4) + 4*(lane/32) + r%4][lane%32] in register r.
+//   16x16x32: A[i][k] lane i%16, k = 8*(lane/16)+e; B[k][j] lane j%16, same k; C[4*(lane/16)+r][lane%16].
+// Both attention products are computed transposed (S^T = K Q^T and O^T = V^T P^T) so that every lane owns whole
+// query rows (prefill) or query heads (decode): softmax statistics and the O rescale stay inside a lane.
+// The head dimension inside the K tile and in the Q fragments is stored in a permuted "virtual" order that puts
+// each rotation pair (t, t + D/2) into the same 16-byte group: for pair t, the low half goes to virtual column
+// 16*(t/8) + 8*((t%8)/4) + t%4 and the high half four columns later.  Any permutation applied to both Q and K
+// leaves Q K^T unchanged.  The key axis of the V^T tile is permuted inside each group of 16 keys
+// (0-3, 8-11, 4-7, 12-15) so that P leaves the S^T accumulators directly in the B-operand order.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "lazy_attn_internal.h"
+
+namespace lazy {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kSub = 64;  // keys of one loader sub-tile; tile row 0 of a sub-tile is a multiple of 64 in its chunk
+constexpr int kPad = 8;   // bf16 elements of padding per LDS row
+constexpr float kLn2 = 0.69314718055994530942f;
+constexpr double kInvTwoPi = 0.15915494309189533577;
+
+static_assert(kPrefillTileKeys == kSub, "prefill tiles are one loader sub-tile");
+static_assert(kDecodeTileKeys == 2 * kSub, "decode tiles are two loader sub-tiles");
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// theta_t / (2 pi): RoPE frequency of pair t in revolutions per position (original RoPE: base^(-2t/D);
+// RoPE variants pass their own table, Sec. 3.5).
+__device__ __forceinline__ double theta_rev(int t, int d, float base, const float* inv_freq) {
+  const double th = inv_freq ? (double)inv_freq[t] : pow((double)base, -2.0 * (double)t / (double)d);
+  return th * kInvTwoPi;
+}
+
+// (cos, sin) of the angle p * theta for theta given in revolutions: the product and its fractional part in fp64,
+// then one fp32 sincos of the reduced angle.
+__device__ __forceinline__ float2 rope_cs(int p, double rev) {
+  double r = (double)p * rev;
+  r -= floor(r);
+  float s, c;
+  sincospif(2.0f * (float)r, &s, &c);
+  return make_float2(c, s);
+}
+
+// Rotate one pair (x1, x2) = (k[t], k[t + D/2]) by the angle base + delta, given (cos, sin) of each part.
+// Written with explicit fmaf so that every kernel that rotates keys rounds identically.
+__device__ __forceinline__ void rotate_pair(float x1, float x2, float2 cb, float2 cd, float& y1, float& y2) {
+  const float c = fmaf(cb.x, cd.x, -(cb.y * cd.y));
+  const float s = fmaf(cb.y, cd.x, cb.x * cd.y);
+  y1 = fmaf(x1, c, -(x2 * s));
+  y2 = fmaf(x1, s, x2 * c);
+}
+
+// Rotate a query pair at position p (accurate angle per pair).
+__device__ __forceinline__ void rotate_q_pair(float x1, float x2, int p, double rev, float& y1, float& y2) {
+  const float2 cs = rope_cs(p, rev);
+  y1 = fmaf(x1, cs.x, -(x2 * cs.y));
+  y2 = fmaf(x1, cs.y, x2 * cs.x);
+}
+
+struct Rec {
+  int64_t koff, voff;
+  int len, pos, kst, vst;
+};
+
+__device__ __forceinline__ Rec load_rec(const lazy_chunk_t* c) {
+  Rec r;
+  r.koff = c->k_offset;
+  r.voff = c->v_offset;
+  r.len = c->len;
+  r.pos = c->pos_offset;
+  r.kst = c->k_stride;
+  r.vst = c->v_stride;
+  return r;
+}
+
+// Walks the key tiles of one request that belong to one KV split: tiles never straddle chunks; the request's
+// tiles (chunk after chunk, TK keys each, the last one of a chunk possibly partial) are numbered and split
+// evenly.  With the causal rule, tiles whose first key lies after the last query of the workgroup are skipped.
+template <int TK>
+struct TileIter {
+  const lazy_chunk_t* recs;
+  int i, end, j0, left;
+  Rec cur;
+
+  __device__ void init(const lazy_chunk_t* chunks, int c0, int c1, int split, int splits) {
+    recs = chunks;
+    end = c1;
+    int ntiles = 0;
+    for (int k = c0; k < c1; ++k) ntiles += (chunks[k].len + TK - 1) / TK;
+    const int lo = (int)((int64_t)ntiles * split / splits);
+    const int hi = (int)((int64_t)ntiles * (split + 1) / splits);
+    left = hi - lo;
+    int acc = 0;
+    i = c0;
+    while (i < c1) {
+      const int nt = (chunks[i].len + TK - 1) / TK;
+      if (acc + nt > lo) break;
+      acc += nt;
+      ++i;
+    }
+    j0 = (lo - acc) * TK;
+    if (left > 0) cur = load_rec(chunks + i);
+  }
+  __device__ void step() {
+    --left;
+    j0 += TK;
+    // Zero-length records own no tile, so while tiles are left a record with keys lies ahead.
+    while (left > 0 && j0 >= cur.len) {
+      ++i;
+      j0 = 0;
+      cur = load_rec(recs + i);
+    }
+  }
+  // Move to the next tile that some query of the workgroup can see (the current one included).
+  __device__ bool seek(bool causal, int qmax) {
+    while (left > 0) {
+      if (!causal || cur.pos + j0 <= qmax) return true;
+      step();
+    }
+    return false;
+  }
+};
+
+template <int D, int NSUB>
+struct Smem {
+  static constexpr int KEYS = kSub * NSUB;
+  static constexpr int KLD = D + kPad;     // K tile: [KEYS][KLD], head dimension in virtual order
+  static constexpr int VLD = KEYS + kPad;  // V^T tile: [D][VLD], keys permuted within groups of 16
+  uint16_t k[KEYS * KLD] __attribute__((aligned(16)));
+  uint16_t vt[D * VLD] __attribute__((aligned(16)));
+  float2 cs[NSUB][D / 2];                  // cos/sin(b_s theta_t) of the current tile's sub-tile bases
+  double freq[D / 2];                      // theta_t / 2pi
+};
+
+__device__ __forceinline__ int perm4(int x) { return ((x & 1) << 1) | ((x >> 1) & 1); }
+
+// Cooperative tile loader: 256 threads bring NSUB sub-tiles of 64 keys into LDS, rotating K if ROT.
+// K: thread = (row = tid/4, quarter = tid%4) handles pairs t in [quarter*D/8, (quarter+1)*D/8).
+// V: thread = (dim group = tid % (D/8), key group = tid / (D/8)) handles 4 keys x 8 dims.
+template <int D, int NSUB, bool ROT>
+struct Loader {
+  static constexpr int PP = D / 8;
+  static constexpr int NV = PP / 8;
+  static constexpr int VTASKS = (kSub / 4) * (D / 8);
+  using S = Smem<D, NSUB>;
+  u32x4 klo[NSUB][NV], khi[NSUB][NV];
+  u32x4 vr[NSUB][4];
+  float2 csd[ROT ? PP : 1];
+  int tid, row, quarter, vdg, va;
+
+  __device__ void init(int t, const double* freq) {
+    tid = t;
+    row = t >> 2;
+    quarter = t & 3;
+    vdg = t % (D / 8);
+    va = t / (D / 8);
+    if (ROT) {
+#pragma unroll
+      for (int e = 0; e < PP; ++e) csd[e] = rope_cs(row, freq[quarter * PP + e]);
+    }
+  }
+
+  // Global loads of one tile: kbase / vbase = K / V of this head at the tile's first key.
+  __device__ void fetch(const uint16_t* kbase, const uint16_t* vbase, int nvalid) {
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) {
+      const int r = s * kSub + row;
+      if (r < nvalid) {
+        const u32x4* lo = reinterpret_cast<const u32x4*>(kbase + (size_t)r * D + quarter * PP);
+        const u32x4* hi = reinterpret_cast<const u32x4*>(kbase + (size_t)r * D + D / 2 + quarter * PP);
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          klo[s][v] = lo[v];
+          khi[s][v] = hi[v];
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < NV; ++v) klo[s][v] = khi[s][v] = u32x4{0, 0, 0, 0};
+      }
+      if (tid < VTASKS) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int rr = s * kSub + 4 * va + i;
+          vr[s][i] = rr < nvalid ? *reinterpret_cast<const u32x4*>(vbase + (size_t)rr * D + 8 * vdg)
+                                 : u32x4{0, 0, 0, 0};
+        }
+      }
+    }
+  }
+
+  __device__ void store(S& sm) {
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) {
+      uint16_t* krow = sm.k + (s * kSub + row) * S::KLD;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int t0 = quarter * PP + 8 * v;  // first pair of this 8-pair group
+        u32x4 w0, w1;
+        if (ROT) {
+          float yl[8], yh[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const uint32_t wl = klo[s][v][e >> 1], wh = khi[s][v][e >> 1];
+            const float x1 = (e & 1) ? bf_hi(wl) : bf_lo(wl);
+            const float x2 = (e & 1) ? bf_hi(wh) : bf_lo(wh);
+            rotate_pair(x1, x2, sm.cs[s][t0 + e], csd[8 * v + e], yl[e], yh[e]);
+          }
+          w0 = u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yh[0], yh[1]), pack2(yh[2], yh[3])};
+          w1 = u32x4{pack2(yl[4], yl[5]), pack2(yl[6], yl[7]), pack2(yh[4], yh[5]), pack2(yh[6], yh[7])};
+        } else {
+          w0 = u32x4{klo[s][v][0], klo[s][v][1], khi[s][v][0], khi[s][v][1]};
+          w1 = u32x4{klo[s][v][2], klo[s][v][3], khi[s][v][2], khi[s][v][3]};
+        }
+        *reinterpret_cast<u32x4*>(krow + 2 * t0) = w0;
+        *reinterpret_cast<u32x4*>(krow + 2 * t0 + 8) = w1;
+      }
+      if (tid < VTASKS) {
+        const int kk = s * kSub + 4 * va;
+        const int col = (kk & ~15) + 4 * perm4((kk >> 2) & 3);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const u32x2 lo2 = {__builtin_amdgcn_perm(vr[s][1][w], vr[s][0][w], 0x05040100u),
+                             __builtin_amdgcn_perm(vr[s][3][w], vr[s][2][w], 0x05040100u)};
+          const u32x2 hi2 = {__builtin_amdgcn_perm(vr[s][1][w], vr[s][0][w], 0x07060302u),
+                             __builtin_amdgcn_perm(vr[s][3][w], vr[s][2][w], 0x07060302u)};
+          *reinterpret_cast<u32x2*>(sm.vt + (8 * vdg + 2 * w) * S::VLD + col) = lo2;
+          *reinterpret_cast<u32x2*>(sm.vt + (8 * vdg + 2 * w + 1) * S::VLD + col) = hi2;
+        }
+      }
+    }
+  }
+};
+
+template <int D, int NSUB>
+__device__ __forceinline__ void compute_base(Smem<D, NSUB>& sm, int tid, int b0) {
+  for (int e = tid; e < NSUB * (D / 2); e += kThreads) {
+    const int s = e / (D / 2), t = e % (D / 2);
+    sm.cs[s][t] = rope_cs(b0 + s * kSub, sm.freq[t]);
+  }
+}
+
+// Load 4 query pairs (t0..t0+3 with their partners t0+D/2..) of one query row, rotated at position p, as one
+// 8-element MFMA fragment in virtual order [low t0..t0+3, high t0..t0+3].
+template <int D>
+__device__ __forceinline__ bf16x8 q_fragment(const uint16_t* qrow, int t0, int p, const double* freq, bool valid) {
+  if (!valid) return as_bf16x8(u32x4{0, 0, 0, 0});
+  const u32x2 lo = *reinterpret_cast<const u32x2*>(qrow + t0);
+  const u32x2 hi = *reinterpret_cast<const u32x2*>(qrow + D / 2 + t0);
+  float y1[4], y2[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float x1 = (e & 1) ? bf_hi(lo[e >> 1]) : bf_lo(lo[e >> 1]);
+    const float x2 = (e & 1) ? bf_hi(hi[e >> 1]) : bf_lo(hi[e >> 1]);
+    rotate_q_pair(x1, x2, p, freq[t0 + e], y1[e], y2[e]);
+  }
+  return as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y2[0], y2[1]), pack2(y2[2], y2[3])});
+}
+
+__device__ __forceinline__ const uint16_t* k_ptr(const uint16_t* pool, const Rec& r, int g, int j0, int d) {
+  return pool + r.koff + ((int64_t)g * r.kst + j0) * d;
+}
+__device__ __forceinline__ const uint16_t* v_ptr(const uint16_t* pool, const Rec& r, int g, int j0, int d) {
+  return pool + r.voff + ((int64_t)g * r.vst + j0) * d;
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Prefill: workgroup = (row tile of 128 packed query rows, KV head, request x split).  Packed row = token * G + g
+// (the G query heads sharing one KV head, Sec. 3.5), four waves x 32 rows, one row per lane pair (lane, lane+32).
+// ---------------------------------------------------------------------------------------------------------------
+template <int D, bool ROT>
+__global__ __launch_bounds__(kThreads) void prefill_kernel(AttnArgs a) {
+  __shared__ Smem<D, 1> sm;
+  using S = Smem<D, 1>;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = blockIdx.y;
+  const int r = blockIdx.z / a.splits, split = blockIdx.z % a.splits;
+  const int qs = a.q_start[r], qe = a.q_start[r + 1];
+  const int G = a.group;
+  const int nrows = (qe - qs) * G;
+  const int row0 = blockIdx.x * kPrefillRows;
+  if (row0 >= nrows) return;
+  const int qp0 = a.q_pos0[r];
+
+  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_base, a.inv_freq);
+  __syncthreads();
+
+  const int h2 = lane >> 5;
+  const int prow = row0 + wave * 32 + (lane & 31);
+  const bool rvalid = prow < nrows;
+  const int tok = rvalid ? prow / G : 0;
+  const int head = g * G + (rvalid ? prow % G : 0);
+  const int qpos = qp0 + tok;
+  const int last = min(row0 + kPrefillRows, nrows) - 1;
+  const int qmin = qp0 + row0 / G, qmax = qp0 + last / G;
+
+  bf16x8 qf[D / 16];
+  {
+    const uint16_t* qrow = a.q + ((int64_t)(qs + tok) * a.hq + head) * D;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) qf[s] = q_fragment<D>(qrow, 8 * s + 4 * h2, qpos, sm.freq, rvalid);
+  }
+
+  f32x16 o[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) o[db] = f32x16{};
+  float m2 = -INFINITY, lsum = 0.f;
+  const float c = a.scale_log2;
+
+  Loader<D, 1, ROT> ld;
+  ld.init(tid, sm.freq);
+  TileIter<kSub> it;
+  it.init(a.chunks, a.chunk_start[r], a.chunk_start[r + 1], split, a.splits);
+  bool have = it.seek(a.causal, qmax);
+  if (have) ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+                     min(kSub, it.cur.len - it.j0));
+  while (have) {
+    const int nvalid = min(kSub, it.cur.len - it.j0);
+    const int b0 = it.cur.pos + it.j0;
+    it.step();
+    const bool have_next = it.seek(a.causal, qmax);
+    if (ROT) compute_base<D, 1>(sm, tid, b0);
+    __syncthreads();
+    ld.store(sm);
+    __syncthreads();
+    if (have_next)
+      ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+               min(kSub, it.cur.len - it.j0));
+
+    // S^T = K Q^T: two 32-key blocks.
+    f32x16 sa[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) {
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) {
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(sm.k + (32 * blk + (lane & 31)) * S::KLD + 16 * s + 8 * h2);
+        sa[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[s], sa[blk], 0, 0, 0);
+      }
+    }
+    if (nvalid < kSub || (a.causal && b0 + kSub - 1 > qmin)) {
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int kk = 32 * blk + 8 * (i >> 2) + 4 * h2 + (i & 3);
+          const bool ok = kk < nvalid && (!a.causal || b0 + kk <= qpos);
+          if (!ok) sa[blk][i] = -INFINITY;
+        }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sa[blk][i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(m2, mx * c);
+    const float muse = mnew == -INFINITY ? 0.f : mnew;
+    const float alpha = fast_exp2(m2 - muse);
+    float ps = 0.f;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float p = fast_exp2(fmaf(sa[blk][i], c, -muse));
+        sa[blk][i] = p;
+        ps += p;
+      }
+    lsum = fmaf(lsum, alpha, ps);
+    m2 = mnew;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) o[db] *= alpha;
+
+    // O^T += V^T P^T: four 16-key steps.
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2) {
+      const f32x16& sv = sa[s2 >> 1];
+      const int b = 8 * (s2 & 1);
+      const bf16x8 pb = as_bf16x8(u32x4{pack2(sv[b + 0], sv[b + 1]), pack2(sv[b + 2], sv[b + 3]),
+                                        pack2(sv[b + 4], sv[b + 5]), pack2(sv[b + 6], sv[b + 7])});
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const u32x4 vv =
+            *reinterpret_cast<const u32x4*>(sm.vt + (32 * db + (lane & 31)) * S::VLD + 16 * s2 + 8 * h2);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pb, o[db], 0, 0, 0);
+      }
+    }
+    have = have_next;
+  }
+
+  const float ltot = lsum + __shfl_xor(lsum, 32);
+  if (!rvalid) return;
+  const int64_t orow = (int64_t)(qs + tok) * a.hq + head;
+  if (a.splits == 1) {
+    const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
+    uint16_t* dst = a.out + orow * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int dim = 32 * db + 8 * q4 + 4 * h2;
+        *reinterpret_cast<u32x2*>(dst + dim) =
+            u32x2{pack2(o[db][4 * q4] * inv, o[db][4 * q4 + 1] * inv),
+                  pack2(o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv)};
+      }
+    if (a.lse && h2 == 0) a.lse[orow] = ltot > 0.f ? (m2 + log2f(ltot)) * kLn2 : -INFINITY;
+  } else {
+    const int64_t wrow = (int64_t)split * a.total_q * a.hq + orow;
+    float* dst = a.ws_acc + wrow * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int dim = 32 * db + 8 * q4 + 4 * h2;
+        *reinterpret_cast<f32x4*>(dst + dim) =
+            f32x4{o[db][4 * q4], o[db][4 * q4 + 1], o[db][4 * q4 + 2], o[db][4 * q4 + 3]};
+      }
+    if (h2 == 0) {
+      a.ws_ml[2 * wrow] = m2 * kLn2;
+      a.ws_ml[2 * wrow + 1] = ltot;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Decode: workgroup = (KV split, KV head x head group, request).  Tiles of 128 keys; wave w owns keys
+// 32w..32w+31 of each tile and keeps its own softmax state for up to 16 query heads (one head per MFMA column);
+// the four waves are merged through LDS at the end.  Rows of the 16x16 S^T blocks map to tile keys through
+// kappa(b, r) = 16*(r/8) + r%8 + 8b so that each lane's eight probabilities are, in order, the eight keys the
+// V^T tile holds at its virtual key positions.
+// ---------------------------------------------------------------------------------------------------------------
+__device__ __forceinline__ int kappa(int b, int r) { return 16 * (r >> 3) + (r & 7) + 8 * b; }
+
+template <int D, bool ROT>
+__global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
+  __shared__ Smem<D, 2> sm;
+  using S = Smem<D, 2>;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int split = blockIdx.x;
+  const int g = blockIdx.y / a.head_groups, hg = blockIdx.y % a.head_groups;
+  const int r = blockIdx.z;
+  const int G = a.group;
+  const int hcount = min(kDecodeHeadsPerGroup, G - kDecodeHeadsPerGroup * hg);
+  const int col = lane & 15, kq = lane >> 4;
+  const int qpos = a.q_pos0[r];
+
+  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_base, a.inv_freq);
+  __syncthreads();
+
+  const bool hvalid = col < hcount;
+  const int head = g * G + kDecodeHeadsPerGroup * hg + (hvalid ? col : 0);
+  bf16x8 qf[D / 32];
+  {
+    const uint16_t* qrow = a.q + ((int64_t)r * a.hq + head) * D;
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s)
+      qf[s] = q_fragment<D>(qrow, 8 * (2 * s + (kq >> 1)) + 4 * (kq & 1), qpos, sm.freq, hvalid);
+  }
+
+  f32x4 o[D / 16];
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) o[db] = f32x4{};
+  float m2 = -INFINITY, lsum = 0.f;
+  const float c = a.scale_log2;
+
+  Loader<D, 2, ROT> ld;
+  ld.init(tid, sm.freq);
+  TileIter<2 * kSub> it;
+  it.init(a.chunks, a.chunk_start[r], a.chunk_start[r + 1], split, a.splits);
+  bool have = it.seek(a.causal, qpos);
+  if (have) ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+                     min(2 * kSub, it.cur.len - it.j0));
+  while (have) {
+    const int nvalid = min(2 * kSub, it.cur.len - it.j0);
+    const int b0 = it.cur.pos + it.j0;
+    it.step();
+    const bool have_next = it.seek(a.causal, qpos);
+    if (ROT) compute_base<D, 2>(sm, tid, b0);
+    __syncthreads();
+    ld.store(sm);
+    __syncthreads();
+    if (have_next)
+      ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+               min(2 * kSub, it.cur.len - it.j0));
+
+    f32x4 sa[2] = {f32x4{}, f32x4{}};
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s) {
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int key = 32 * wave + kappa(b, col);
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(sm.k + key * S::KLD + 32 * s + 8 * kq);
+        sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kv), qf[s], sa[b], 0, 0, 0);
+      }
+    }
+    if (nvalid < 2 * kSub || (a.causal && b0 + 2 * kSub - 1 > qpos)) {
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kk = 32 * wave + kappa(b, 4 * kq + i);
+          const bool ok = kk < nvalid && (!a.causal || b0 + kk <= qpos);
+          if (!ok) sa[b][i] = -INFINITY;
+        }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sa[b][i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(m2, mx * c);
+    const float muse = mnew == -INFINITY ? 0.f : mnew;
+    const float alpha = fast_exp2(m2 - muse);
+    float ps = 0.f;
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = fast_exp2(fmaf(sa[b][i], c, -muse));
+        sa[b][i] = p;
+        ps += p;
+      }
+    lsum = fmaf(lsum, alpha, ps);
+    m2 = mnew;
+    const bf16x8 pb = as_bf16x8(u32x4{pack2(sa[0][0], sa[0][1]), pack2(sa[0][2], sa[0][3]),
+                                      pack2(sa[1][0], sa[1][1]), pack2(sa[1][2], sa[1][3])});
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+      o[db] *= alpha;
+      const u32x4 vv = *reinterpret_cast<const u32x4*>(sm.vt + (16 * db + col) * S::VLD + 32 * wave + 8 * kq);
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vv), pb, o[db], 0, 0, 0);
+    }
+    have = have_next;
+  }
+
+  // Merge the four waves' states through LDS (the K tile area is free now).
+  float ltot = lsum + __shfl_xor(lsum, 16);
+  ltot += __shfl_xor(ltot, 32);
+  __syncthreads();
+  float* macc = reinterpret_cast<float*>(sm.k);  // [4][D][16]
+  float* mm = macc + 4 * D * 16;                 // [4][16]
+  float* ml = mm + 4 * 16;                       // [4][16]
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) macc[(wave * D + 16 * db + 4 * kq + i) * 16 + col] = o[db][i];
+  if (kq == 0) {
+    mm[wave * 16 + col] = m2;
+    ml[wave * 16 + col] = ltot;
+  }
+  __syncthreads();
+  for (int idx = tid; idx < 16 * (D / 4); idx += kThreads) {
+    const int hc = idx & 15, d4 = idx >> 4;
+    if (hc >= hcount) continue;
+    float mw[4], mmax = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      mw[w] = mm[w * 16 + hc];
+      mmax = fmaxf(mmax, mw[w]);
+    }
+    float l = 0.f;
+    f32x4 acc = f32x4{};
+    if (mmax != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float sc = fast_exp2(mw[w] - mmax);
+        l = fmaf(ml[w * 16 + hc], sc, l);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] = fmaf(macc[(w * D + 4 * d4 + e) * 16 + hc], sc, acc[e]);
+      }
+    }
+    const int hh = g * G + kDecodeHeadsPerGroup * hg + hc;
+    const int64_t orow = (int64_t)r * a.hq + hh;
+    if (a.splits == 1) {
+      const float inv = l > 0.f ? 1.f / l : 0.f;
+      *reinterpret_cast<u32x2*>(a.out + orow * D + 4 * d4) =
+          u32x2{pack2(acc[0] * inv, acc[1] * inv), pack2(acc[2] * inv, acc[3] * inv)};
+      if (a.lse && d4 == 0) a.lse[orow] = l > 0.f ? (mmax + log2f(l)) * kLn2 : -INFINITY;
+    } else {
+      const int64_t wrow = (int64_t)split * a.total_q * a.hq + orow;
+      *reinterpret_cast<f32x4*>(a.ws_acc + wrow * D + 4 * d4) = acc;
+      if (d4 == 0) {
+        a.ws_ml[2 * wrow] = mmax * kLn2;
+        a.ws_ml[2 * wrow + 1] = l;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Split-KV combine: out = sum_s e^{m_s - M} acc_s / sum_s e^{m_s - M} l_s.  D/4 threads per row, 4 dims each.
+// ---------------------------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kThreads) void combine_kernel(const float* __restrict__ acc,
+                                                           const float* __restrict__ ml, int splits, int rows,
+                                                           uint16_t* __restrict__ out, float* __restrict__ lse) {
+  constexpr int TPR = D / 4;
+  const int row = blockIdx.x * (kThreads / TPR) + threadIdx.x / TPR;
+  const int d4 = threadIdx.x % TPR;
+  if (row >= rows) return;
+  float mmax = -INFINITY;
+  for (int s = 0; s < splits; ++s) mmax = fmaxf(mmax, ml[2 * ((int64_t)s * rows + row)]);
+  float l = 0.f;
+  f32x4 sum = f32x4{};
+  if (mmax != -INFINITY) {
+    for (int s = 0; s < splits; ++s) {
+      const int64_t w = (int64_t)s * rows + row;
+      const float m = ml[2 * w];
+      if (m == -INFINITY) continue;
+      const float sc = expf(m - mmax);
+      l = fmaf(ml[2 * w + 1], sc, l);
+      const f32x4 v = *reinterpret_cast<const f32x4*>(acc + w * D + 4 * d4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum[e] = fmaf(v[e], sc, sum[e]);
+    }
+  }
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  *reinterpret_cast<u32x2*>(out + (int64_t)row * D + 4 * d4) =
+      u32x2{pack2(sum[0] * inv, sum[1] * inv), pack2(sum[2] * inv, sum[3] * inv)};
+  if (lse && d4 == 0) lse[row] = l > 0.f ? mmax + logf(l) : -INFINITY;
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Materialise-then-attend baseline.
+// ---------------------------------------------------------------------------------------------------------------
+// Plan: exclusive prefix sum of record lengths -> records describing the contiguous rotated copy.
+__global__ __launch_bounds__(kThreads) void materialize_plan_kernel(const lazy_chunk_t* in, int n, int hkv, int d,
+                                                                    lazy_chunk_t* out) {
+  __shared__ int64_t scan[kThreads];
+  const int tid = threadIdx.x;
+  int64_t carry = 0;
+  for (int base = 0; base < n; base += kThreads) {
+    const int i = base + tid;
+    const int64_t len = i < n ? in[i].len : 0;
+    scan[tid] = len;
+    __syncthreads();
+    for (int off = 1; off < kThreads; off <<= 1) {
+      const int64_t add = tid >= off ? scan[tid - off] : 0;
+      __syncthreads();
+      scan[tid] += add;
+      __syncthreads();
+    }
+    if (i < n) {
+      lazy_chunk_t rec = in[i];
+      rec.k_offset = (scan[tid] - len + carry) * hkv * d;
+      rec.k_stride = rec.len;
+      out[i] = rec;
+    }
+    carry += scan[kThreads - 1];
+    __syncthreads();
+  }
+}
+
+// Rotate-and-copy: workgroup = (64-key sub-tile, KV head, record).  Same angle decomposition and rounding as the
+// lazy loader, written back in the natural head-dimension order.
+template <int D>
+__global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint16_t* __restrict__ k_pool,
+                                                                      const lazy_chunk_t* __restrict__ in,
+                                                                      const lazy_chunk_t* __restrict__ plan,
+                                                                      float base, const float* inv_freq,
+                                                                      uint16_t* __restrict__ k_out) {
+  constexpr int PP = D / 8, NV = PP / 8;
+  __shared__ double freq[D / 2];
+  __shared__ float2 cs[D / 2];
+  const int tid = threadIdx.x;
+  const Rec rc = load_rec(in + blockIdx.z);
+  const int g = blockIdx.y, j0 = blockIdx.x * kSub;
+  if (j0 >= rc.len) return;
+  if (tid < D / 2) {
+    freq[tid] = theta_rev(tid, D, base, inv_freq);
+    cs[tid] = rope_cs(rc.pos + j0, freq[tid]);
+  }
+  __syncthreads();
+  const int row = tid >> 2, quarter = tid & 3;
+  if (j0 + row >= rc.len) return;
+  const uint16_t* src = k_ptr(k_pool, rc, g, j0 + row, D);
+  uint16_t* dst = k_out + plan[blockIdx.z].k_offset + ((int64_t)g * rc.len + j0 + row) * D;
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int t0 = quarter * PP + 8 * v;
+    const u32x4 wl = *reinterpret_cast<const u32x4*>(src + t0);
+    const u32x4 wh = *reinterpret_cast<const u32x4*>(src + D / 2 + t0);
+    float yl[8], yh[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float x1 = (e & 1) ? bf_hi(wl[e >> 1]) : bf_lo(wl[e >> 1]);
+      const float x2 = (e & 1) ? bf_hi(wh[e >> 1]) : bf_lo(wh[e >> 1]);
+      rotate_pair(x1, x2, cs[t0 + e], rope_cs(row, freq[t0 + e]), yl[e], yh[e]);
+    }
+    *reinterpret_cast<u32x4*>(dst + t0) =
+        u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yl[4], yl[5]), pack2(yl[6], yl[7])};
+    *reinterpret_cast<u32x4*>(dst + D / 2 + t0) =
+        u32x4{pack2(yh[0], yh[1]), pack2(yh[2], yh[3]), pack2(yh[4], yh[5]), pack2(yh[6], yh[7])};
+  }
+}
+
+template <int D, bool ROT>
+hipError_t prefill_d(const AttnArgs& a, hipStream_t st) {
+  const dim3 grid(a.q_tiles, a.hkv, a.batch * a.splits);
+  hipLaunchKernelGGL((prefill_kernel<D, ROT>), grid, dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int D, bool ROT>
+hipError_t decode_d(const AttnArgs& a, hipStream_t st) {
+  const dim3 grid(a.splits, a.hkv * a.head_groups, a.batch);
+  hipLaunchKernelGGL((decode_kernel<D, ROT>), grid, dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_combine(const float* acc, const float* ml, int splits, int rows, int head_dim, uint16_t* out,
+                          float* lse, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  const int per_block = kThreads / (head_dim / 4);
+  const dim3 grid((rows + per_block - 1) / per_block);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kThreads), 0, st, acc, ml, splits, rows, out, lse);
+  else
+    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(kThreads), 0, st, acc, ml, splits, rows, out, lse);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t st) {
+  hipError_t e;
+  if (head_dim == 128)
+    e = rotate_k ? prefill_d<128, true>(a, st) : prefill_d<128, false>(a, st);
+  else
+    e = rotate_k ? prefill_d<64, true>(a, st) : prefill_d<64, false>(a, st);
+  if (e != hipSuccess || a.splits == 1) return e;
+  return launch_combine(a.ws_acc, a.ws_ml, a.splits, a.total_q * a.hq, head_dim, a.out, a.lse, st);
+}
+
+hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t st) {
+  hipError_t e;
+  if (head_dim == 128)
+    e = rotate_k ? decode_d<128, true>(a, st) : decode_d<128, false>(a, st);
+  else
+    e = rotate_k ? decode_d<64, true>(a, st) : decode_d<64, false>(a, st);
+  if (e != hipSuccess || a.splits == 1) return e;
+  return launch_combine(a.ws_acc, a.ws_ml, a.splits, a.total_q * a.hq, head_dim, a.out, a.lse, st);
+}
+
+hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
+                              int max_chunk_len, int hkv, int head_dim, float rope_base, const float* inv_freq,
+                              uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t st) {
+  if (num_records <= 0) return hipSuccess;
+  hipLaunchKernelGGL(materialize_plan_kernel, dim3(1), dim3(kThreads), 0, st, chunks, num_records, hkv, head_dim,
+                     chunks_out);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || max_chunk_len <= 0) return e;
+  const dim3 grid((max_chunk_len + kSub - 1) / kSub, hkv, num_records);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(materialize_rotate_kernel<128>, grid, dim3(kThreads), 0, st, k_pool, chunks, chunks_out,
+                       rope_base, inv_freq, k_out);
+  else
+    hipLaunchKernelGGL(materialize_rotate_kernel<64>, grid, dim3(kThreads), 0, st, k_pool, chunks, chunks_out,
+                       rope_base, inv_freq, k_out);
+  return hipGetLastError();
+}
+
+}  // namespace lazy

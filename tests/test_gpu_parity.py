@@ -1,0 +1,284 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 oracle, element by element on seeded inputs.
+
+Tolerance (bf16 outputs): max |gpu - oracle| <= 2e-2 and mean |gpu - oracle| <= 2e-3; lse within 2e-2 where finite
+and -inf exactly where the oracle has no visible key.  Lazy (in-kernel rotation) and materialise-then-attend
+compute the same rotated bf16 keys, so they must agree bit for bit.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import lazy_oracle as O
+from paper_2606_04302_amd import ops
+from paper_2606_04302_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS, LSE_ABS = 2e-2, 2e-3, 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ops.lib()
+    torch.cuda.init()
+    yield
+
+
+def oracle(w, requests=None, **kw):
+    if w.kind == "decode":
+        return O.lazy_decode(w.q, w.q_pos0, w.pool, w.pool, w.chunks, w.chunk_start, w.num_q_heads, w.num_kv_heads,
+                             w.head_dim, w.rope_base, w.causal, requests=requests, **kw)
+    return O.lazy_attention(w.q, w.q_start, w.q_pos0, w.pool, w.pool, w.chunks, w.chunk_start, w.num_q_heads,
+                            w.num_kv_heads, w.head_dim, w.rope_base, w.causal, requests=requests, **kw)
+
+
+def rows_of(w, requests):
+    idx = []
+    for r in requests:
+        idx.extend(range(int(w.q_start[r]), int(w.q_start[r + 1])))
+    return np.array(idx, dtype=np.int64)
+
+
+def assert_close(out, lse, ref_o, ref_l, rows=None, tag=""):
+    o = out.float().cpu().numpy().astype(np.float64)
+    l = lse.cpu().numpy().astype(np.float64) if lse is not None else None
+    if rows is not None:
+        o, ref_o = o[rows], ref_o[rows]
+        if l is not None:
+            l, ref_l = l[rows], ref_l[rows]
+    assert np.isfinite(o).all(), f"{tag}: non-finite output"
+    err = np.abs(o - ref_o)
+    print(f"{tag}: max_abs={err.max():.3e} mean_abs={err.mean():.3e} rms_ref={np.sqrt((ref_o ** 2).mean()):.3e}",
+          flush=True)
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, f"{tag}: max {err.max()} mean {err.mean()}"
+    if l is not None:
+        inf = np.isneginf(ref_l)
+        assert np.array_equal(np.isneginf(l), inf), f"{tag}: lse -inf pattern differs"
+        if (~inf).any():
+            le = np.abs(l[~inf] - ref_l[~inf]).max()
+            assert le <= LSE_ABS, f"{tag}: lse err {le}"
+
+
+def run_and_check(w, tag, cfg_kw=None, requests=None):
+    dw = ops.upload(w)
+    cfg = ops.config_of(w, **(cfg_kw or {}))
+    out, lse = ops.run_lazy(dw, cfg)
+    torch.cuda.synchronize()
+    okw = {}
+    if cfg_kw and cfg_kw.get("softmax_scale"):
+        okw["softmax_scale"] = cfg_kw["softmax_scale"]
+    ref_o, ref_l = oracle(w, requests=requests, **okw)
+    rows = None if requests is None else rows_of(w, requests)
+    assert_close(out, lse, ref_o, ref_l, rows, tag)
+    return dw, out, lse
+
+
+# --------------------------------------------------------------------------------------------------------------
+
+
+def test_tiny_rag_prefill_matches_oracle():
+    w = W.tiny_rag_prefill(seed=0)
+    dw, out, lse = run_and_check(w, "tiny bf16")
+    # against the fp32 originals as well (the bf16 rounding of inputs is inside the tolerance)
+    ref_o, _ = O.lazy_attention(w.q_fp32, w.q_start, w.q_pos0, w.pool_fp32, w.pool_fp32, w.chunks, w.chunk_start,
+                                w.num_q_heads, w.num_kv_heads, w.head_dim, w.rope_base, w.causal)
+    err = np.abs(out.float().cpu().numpy() - ref_o)
+    print(f"tiny vs fp32 originals: max_abs={err.max():.3e} mean_abs={err.mean():.3e}")
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
+
+
+PREFILL_CASES = {
+    # name: (builder, kwargs, cfg kwargs)
+    "rag_d128_g4": (W.rag_prefill, dict(seed=11, batch=2, hq=8, hkv=2, d=128, prefix_len=40, n_chunks=3,
+                                        chunk_len=100, pool_chunks=5, q_len=37), {}),
+    "rag_d64_g2_split3": (W.rag_prefill, dict(seed=12, batch=3, hq=4, hkv=2, d=64, prefix_len=0, n_chunks=4,
+                                              chunk_len=70, pool_chunks=6, q_len=50), dict(num_splits=3)),
+    "rag_d128_g1_split1": (W.rag_prefill, dict(seed=13, batch=2, hq=2, hkv=2, d=128, prefix_len=17, n_chunks=2,
+                                               chunk_len=64, pool_chunks=3, q_len=129), dict(num_splits=1)),
+    "varlen_g7": (W.varlen_rag, dict(seed=14, batch=4, hq=28, hkv=4, d=128, pool_chunks=10, len_lo=1, len_hi=200,
+                                     k_lo=2, k_hi=5, q_lo=1, q_hi=40), {}),
+    "varlen_g8_d64": (W.varlen_rag, dict(seed=15, batch=3, hq=16, hkv=2, d=64, pool_chunks=8, len_lo=30,
+                                         len_hi=300, k_lo=1, k_hi=4, q_lo=20, q_hi=70), dict(num_splits=2)),
+    "icl_small": (W.icl_prefill, dict(seed=16, batch=2, hq=8, hkv=2, d=128, n_chunks=12, chunk_len=32, q_len=80,
+                                      decode_steps=4), {}),
+}
+
+
+@pytest.mark.parametrize("name", list(PREFILL_CASES))
+def test_prefill_matches_oracle(name):
+    fn, kw, ckw = PREFILL_CASES[name]
+    run_and_check(fn(**kw), name, ckw)
+
+
+def test_prefill_non_causal_and_scale_override():
+    w = W.rag_prefill(seed=21, batch=2, hq=8, hkv=4, d=128, prefix_len=8, n_chunks=2, chunk_len=90, pool_chunks=4,
+                      q_len=20)
+    w.causal = False
+    run_and_check(w, "non-causal")
+    w.causal = True
+    run_and_check(w, "scale 0.05", dict(softmax_scale=0.05))
+
+
+DECODE_CASES = {
+    "d128_g4": (dict(seed=31, batch=3, hq=8, hkv=2, d=128, n_chunks=5, chunk_len=200, pool_chunks=7, tail_len=9,
+                     tail_cap=16), {}),
+    "d128_g4_split1": (dict(seed=32, batch=2, hq=8, hkv=2, d=128, n_chunks=3, chunk_len=130, pool_chunks=4,
+                            tail_len=1, tail_cap=8), dict(num_splits=1)),
+    "d64_g7_split5": (dict(seed=33, batch=2, hq=14, hkv=2, d=64, n_chunks=4, chunk_len=150, pool_chunks=5,
+                           tail_len=33, tail_cap=40), dict(num_splits=5)),
+    "d128_g20_two_head_groups": (dict(seed=34, batch=2, hq=40, hkv=2, d=128, n_chunks=2, chunk_len=300,
+                                      pool_chunks=3, tail_len=5, tail_cap=8), {}),
+    "d128_mha": (dict(seed=35, batch=2, hq=4, hkv=4, d=128, n_chunks=2, chunk_len=257, pool_chunks=3, tail_len=2,
+                      tail_cap=2), dict(num_splits=2)),
+}
+
+
+@pytest.mark.parametrize("name", list(DECODE_CASES))
+def test_decode_matches_oracle(name):
+    kw, ckw = DECODE_CASES[name]
+    run_and_check(W.rag_decode(**kw), "decode " + name, ckw)
+
+
+@pytest.mark.parametrize("kind", ["prefill", "decode"])
+def test_lazy_equals_materialize_then_attend_bitwise(kind):
+    if kind == "prefill":
+        w = W.rag_prefill(seed=41, batch=3, hq=8, hkv=2, d=128, prefix_len=30, n_chunks=3, chunk_len=150,
+                          pool_chunks=5, q_len=70)
+    else:
+        w = W.rag_decode(seed=42, batch=3, hq=8, hkv=2, d=128, n_chunks=4, chunk_len=190, pool_chunks=6,
+                         tail_len=7, tail_cap=12)
+    dw = ops.upload(w)
+    out_l, lse_l = ops.run_lazy(dw)
+    (out_m, lse_m), (k_out, ch_out) = ops.run_materialized(dw)
+    torch.cuda.synchronize()
+    assert torch.equal(out_l.view(torch.int16), out_m.view(torch.int16))
+    assert torch.equal(lse_l, lse_m)
+
+
+def test_materialized_keys_match_oracle():
+    w = W.rag_prefill(seed=43, batch=2, hq=4, hkv=2, d=128, prefix_len=10, n_chunks=2, chunk_len=77, pool_chunks=3,
+                      q_len=5)
+    dw = ops.upload(w)
+    cfg = dw.cfg
+    total = int(w.chunks["len"].astype(np.int64).sum())
+    k_out, ch_out = ops.materialize_k(cfg, dw.pool, dw.chunks, int(w.chunks["len"].max()), total)
+    torch.cuda.synchronize()
+    recs = ops.chunks_from_tensor(ch_out)
+    ref = O.materialize_k(w.pool, w.chunks, w.chunk_start, 2, 128, w.rope_base)
+    got = k_out.float().cpu().numpy()
+    base = 0
+    for r in range(w.batch):
+        a, b = int(w.chunk_start[r]), int(w.chunk_start[r + 1])
+        assert int(recs[a]["k_offset"]) == base
+        start = 0
+        for i in range(a, b):
+            n = int(recs[i]["len"])
+            assert int(recs[i]["k_stride"]) == n and int(recs[i]["v_offset"]) == int(w.chunks[i]["v_offset"])
+            blk = got[int(recs[i]["k_offset"]): int(recs[i]["k_offset"]) + 2 * n * 128].reshape(2, n, 128)
+            # one bf16 rounding of an fp32 rotation: relative error <= 2^-8 plus fp32 angle error
+            np.testing.assert_allclose(blk, ref[r][:, start:start + n], rtol=2 ** -8, atol=1e-5)
+            start += n
+            base += 2 * n * 128
+
+
+def test_combine_entry_point_matches_oracle_merge():
+    rng = np.random.default_rng(5)
+    s, rows, d = 5, 37, 128
+    m = rng.normal(0, 3, size=(s, rows))
+    m[1, :4] = -np.inf  # empty splits
+    m[:, 7] = -np.inf   # a row with no key at all
+    l = np.where(np.isfinite(m), rng.uniform(1, 50, size=(s, rows)), 0.0)
+    acc = np.where(np.isfinite(m)[..., None], rng.normal(size=(s, rows, d)), 0.0)
+    ref_o, ref_l = O.merge_partials(m, l, acc)
+    ml = torch.tensor(np.stack([m, l], -1), dtype=torch.float32, device="cuda")
+    ta = torch.tensor(acc, dtype=torch.float32, device="cuda")
+    lse = torch.empty(rows, dtype=torch.float32, device="cuda")
+    out, _ = ops.combine(ta, ml, lse=lse)
+    torch.cuda.synchronize()
+    assert_close(out, lse, ref_o, ref_l, tag="combine")
+
+
+def test_edge_cases_empty_request_no_visible_key_len1_chunks_nan_slack():
+    reqs = [
+        dict(chunks=[(5, 100)], q_len=3, q_pos0=2),                        # keys after every query: none visible
+        dict(chunks=[(1, 0), (1, 1), (1, 2), ("s", 65, 3)], q_len=0, q_pos0=68),  # no query tokens
+        dict(chunks=[("s", 65, 10), (1, 80), (130, 81)], q_len=64, q_pos0=150),
+        dict(chunks=[], q_len=2, q_pos0=0),                                # no chunk at all
+        dict(chunks=[(1, 0)], q_len=1, q_pos0=0),                          # single key
+    ]
+    w = W.custom(51, 8, 2, 128, 1e4, reqs, slack_fill=np.nan)
+    run_and_check(w, "edge prefill")
+    run_and_check(w, "edge prefill split4", dict(num_splits=4))
+    wd = W.rag_decode(seed=52, batch=2, hq=8, hkv=2, d=128, n_chunks=2, chunk_len=64, pool_chunks=3, tail_len=3,
+                      tail_cap=64, slack_fill=np.nan)
+    run_and_check(wd, "edge decode NaN slack")
+
+
+def test_store_is_read_only():
+    w = W.rag_prefill(seed=61, batch=4, hq=8, hkv=2, d=128, prefix_len=20, n_chunks=3, chunk_len=64, pool_chunks=3,
+                      q_len=16)
+    dw = ops.upload(w)
+    before = dw.pool.clone()
+    ops.run_lazy(dw)
+    ops.run_materialized(dw)
+    torch.cuda.synchronize()
+    assert torch.equal(before.view(torch.int16), dw.pool.view(torch.int16))
+
+
+def test_position_discrimination():
+    """Off-by-one position bugs cannot hide under the tolerance: on short chunks that each carry real attention
+    mass, the GPU result of every request is far closer (in mean error) to the oracle than to the oracle with any
+    one of its chunks moved by one position.  (CPU emulation of the bf16 rounding puts the margin at ~30x.)"""
+    reqs = [dict(chunks=[(24, 5 + 37 * r), (24, 300 + 11 * r), (4, 400 + 3 * r)], q_len=4, q_pos0=400 + 3 * r)
+            for r in range(4)]
+    w = W.custom(71, 4, 2, 128, 1e4, reqs)
+    dw = ops.upload(w)
+    out, _ = ops.run_lazy(dw)
+    torch.cuda.synchronize()
+    o = out.float().cpu().numpy()
+    ref, _ = oracle(w)
+    for i in range(len(w.chunks)):
+        r = int(np.searchsorted(w.chunk_start, i, side="right")) - 1
+        rows = slice(int(w.q_start[r]), int(w.q_start[r + 1]))
+        e0 = np.abs(o[rows] - ref[rows]).mean()
+        for d in (-1, 1):
+            w2 = W.Workload(**{**w.__dict__})
+            w2.chunks = w.chunks.copy()
+            w2.chunks["pos_offset"][i] += d
+            e1 = np.abs(o[rows] - oracle(w2)[0][rows]).mean()
+            assert e1 > 8 * e0, (i, d, e0, e1)
+
+
+def test_inv_freq_table_variant():
+    w = W.rag_prefill(seed=81, batch=2, hq=8, hkv=2, d=128, prefix_len=8, n_chunks=2, chunk_len=100, pool_chunks=3,
+                      q_len=12)
+    # a scaled table (every frequency divided by 4, NTK-like) passed explicitly
+    theta = (np.power(5.0e5, -2.0 * np.arange(64) / 128) / 4.0).astype(np.float32)
+    dw = ops.upload(w)
+    cfg = ops.config_of(w, inv_freq=torch.tensor(theta, device="cuda"))
+    out, lse = ops.run_lazy(dw, cfg)
+    torch.cuda.synchronize()
+    ref_o, ref_l = O.lazy_attention(w.q, w.q_start, w.q_pos0, w.pool, w.pool, w.chunks, w.chunk_start, 8, 2, 128,
+                                    w.rope_base, True, inv_freq=theta.astype(np.float64))
+    assert_close(out, lse, ref_o, ref_l, tag="inv_freq")
+
+
+# Full sizes, default launch configuration (the one the benchmark times); the oracle checks sampled requests.
+FULL = {
+    "rag_prefill": (lambda: W.rag_prefill(seed=1), [0, 5]),
+    "rag_decode": (lambda: W.rag_decode(seed=2), [0, 37, 63]),
+    "icl_prefill": (lambda: W.icl_prefill(seed=3), [2]),
+    "varlen_rag": (lambda: W.varlen_rag(seed=4), [0, 9, 15]),
+}
+
+
+@pytest.mark.parametrize("name", list(FULL))
+def test_full_size_sampled(name):
+    make, reqs = FULL[name]
+    w = make()
+    print(f"{name}: batch={w.batch} total_q={w.total_q} max_kv={w.max_kv_len} meta={w.meta}", flush=True)
+    run_and_check(w, "full " + name, requests=reqs)
