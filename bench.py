@@ -1,0 +1,297 @@
+#!/usr/bin/env python3
+"""Benchmark of the LazyAttention hot path on one MI355X.
+
+Headline (the JSON line's ``value``): lazy prefill of the Llama-3-8B-shaped RAG batch (B=8, 32 query / 8 KV heads,
+head_dim 128, RoPE base 5e5, shared 128-token prefix + 10 retrieved 512-token chunks from a 64-chunk pool at
+per-request positions + a 64-token causal question), in useful TFLOP/s with inputs resident in HBM.  One step is
+one ``lazy_attn_prefill`` call (prefill kernel + split-KV combine).  The same line carries the split-KV decode
+(B=64, ~16.5K position-free keys per request, chunks shared across requests at different offsets) in logical HBM
+GB/s, the materialise-then-attend baseline for both, a no-rotation diagnostic, the roofline of the dominant
+kernel and the fp64 oracle timed on the host cores.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "RAG prefill ms & TFLOP/s (MFMA %), decode HBM GB/s, vs materialize baseline"
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0     # MI355X HBM3E
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_04302_amd", "csrc", "lazy_attn_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def kernel_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def recorded_traffic(kernel: str):
+    """HBM bytes per launch measured with rocprofv3 --pmc (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known
+    size); null when the kernel source changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = rec.get(kernel)
+    if not entry or entry.get("kernel_source_sha256_16") != kernel_hash():
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def timed(fn, steps: int, warmup: int):
+    """Average ms per call, measured with HIP events on the current stream around ``steps`` back-to-back calls."""
+    import torch
+
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        fn()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def cpu_baseline(w, flops_per_pass: float, budget_s: float = 12.0):
+    """The fp64 oracle on the host cores, whole passes over the same batch until ``budget_s`` has elapsed."""
+    from oracle import lazy_oracle as O
+
+    try:
+        import threadpoolctl
+
+        threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
+    except Exception:  # pragma: no cover - informational only
+        threads = os.cpu_count() or 1
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        O.lazy_attention(w.q, w.q_start, w.q_pos0, w.pool, w.pool, w.chunks, w.chunk_start, w.num_q_heads,
+                         w.num_kv_heads, w.head_dim, w.rope_base, w.causal)
+        passes += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or passes >= 50:
+            break
+    per = el / passes
+    return {
+        "value": flops_per_pass / per / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"full rag_prefill batch (8 requests), {passes} pass(es), {per:.2f} s per pass, numpy fp64",
+        "s_per_pass": per,
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode and baseline legs")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (reference kernel for HBM counters)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported (the hot path shards by "
+              "request / KV head without communication, see DESIGN.md)", file=sys.stderr)
+        return 2
+    rank = int(os.environ.get("RANK", "0"))
+
+    import torch
+
+    from paper_2606_04302_amd import accounting as A
+    from paper_2606_04302_amd import ops
+    from paper_2606_04302_amd import workloads as W
+
+    ops.lib()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    # ---------------- prefill (headline) ----------------
+    log("prefill workload: generating")
+    wp = W.rag_prefill(seed=1)
+    dp = ops.upload(wp, dev)
+    cfg = dp.cfg
+    flops = A.useful_flops(wp)
+    alg_bytes = A.algorithmic_bytes(wp)
+    ws_bytes = ops.prefill_workspace_size(cfg, wp.batch, wp.total_q, wp.max_q_len, wp.max_kv_len)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
+    out = torch.empty_like(dp.q)
+    lse = torch.empty((wp.total_q, wp.num_q_heads), dtype=torch.float32, device=dev)
+
+    def prefill():
+        ops.prefill(cfg, dp.q, dp.q_start, dp.q_pos0, dp.pool, dp.pool, dp.chunks, dp.chunk_start, wp.max_q_len,
+                    wp.max_kv_len, out=out, lse=lse, workspace=ws)
+
+    torch.cuda.synchronize()
+    log(f"prefill: timing {args.steps} steps after {args.warmup} warmup")
+    ms = timed(prefill, args.steps, args.warmup)
+
+    # The combine kernel alone on the same partials, to isolate the prefill kernel's own duration.
+    splits = ws_bytes // (wp.total_q * wp.num_q_heads * (wp.head_dim + 2) * 4) if ws_bytes else 1
+    combine_ms = 0.0
+    if splits > 1:
+        rows = wp.total_q * wp.num_q_heads
+        wsf = ws.view(torch.float32)
+        acc = wsf[: splits * rows * wp.head_dim].view(splits, rows, wp.head_dim)
+        ml = wsf[splits * rows * wp.head_dim: splits * rows * (wp.head_dim + 2)].view(splits, rows, 2)
+        out2 = torch.empty((rows, wp.head_dim), dtype=torch.bfloat16, device=dev)
+        lse2 = torch.empty(rows, dtype=torch.float32, device=dev)
+        combine_ms = timed(lambda: ops.combine(acc, ml, out=out2, lse=lse2), args.steps, args.warmup)
+    kernel_ms = ms - combine_ms
+
+    # No-rotation diagnostic: the same kernel with K rotation compiled out, over the unrotated store.
+    norot_ms = timed(lambda: ops.prefill(cfg, dp.q, dp.q_start, dp.q_pos0, dp.pool, dp.pool, dp.chunks,
+                                         dp.chunk_start, wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws,
+                                         plain=True), args.steps, args.warmup)
+
+    # Materialise-then-attend baseline: rotate-and-copy K, then plain attention over the copy.
+    total_kv = int(wp.chunks["len"].astype(np.int64).sum())
+    k_mat = torch.empty(cfg.num_kv_heads * total_kv * cfg.head_dim, dtype=torch.bfloat16, device=dev)
+    ch_mat = torch.empty_like(dp.chunks)
+    max_chunk = int(wp.chunks["len"].max())
+    mat_ms = timed(lambda: ops.materialize_k(cfg, dp.pool, dp.chunks, max_chunk, total_kv, k_out=k_mat,
+                                             chunks_out=ch_mat), args.steps, args.warmup)
+    plain_ms = timed(lambda: ops.prefill(cfg, dp.q, dp.q_start, dp.q_pos0, k_mat, dp.pool, ch_mat, dp.chunk_start,
+                                         wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws, plain=True),
+                     args.steps, args.warmup)
+
+    tflops = flops / (ms * 1e-3) / 1e12
+    kernel_tflops = flops / (kernel_ms * 1e-3) / 1e12
+    result = {
+        "metric": METRIC,
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "rag_prefill: Llama-3-8B-shaped RAG prefill, batch 8, 32 query / 8 KV heads, head_dim 128, "
+                        "RoPE base 5e5, 128-token shared prefix + 10 x 512-token chunks drawn from a 64-chunk pool "
+                        "(random order, contiguous positions) + 64-token causal question",
+            "batch": wp.batch,
+            "q_tokens": wp.total_q,
+            "kv_tokens_per_request": int(wp.max_kv_len),
+            "splits": int(splits),
+        },
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(kernel_tflops, 3),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(kernel_tflops / PEAK_BF16_TFLOPS, 5),
+            "traffic": recorded_traffic("prefill_kernel_rag_prefill"),
+            "kernel": "prefill_kernel<128, rotate K>",
+            "kernel_ms": round(kernel_ms, 5),
+            "useful_gflop_per_launch": round(flops / 1e9, 4),
+            "algorithmic_mb_per_launch": round(alg_bytes / 1e6, 3),
+        },
+        "prefill": {
+            "ms": round(ms, 5),
+            "tflops": round(tflops, 3),
+            "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 5),
+            "kernel_ms": round(kernel_ms, 5),
+            "combine_ms": round(combine_ms, 5),
+            "logical_hbm_gbps": round(alg_bytes / (ms * 1e-3) / 1e9, 1),
+            "no_rotation_ms": round(norot_ms, 5),
+            "rotation_overhead": round(ms / norot_ms - 1.0, 4),
+            "materialize_ms": round(mat_ms, 5),
+            "plain_attention_ms": round(plain_ms, 5),
+            "materialize_then_attend_ms": round(mat_ms + plain_ms, 5),
+            "speedup_vs_materialize": round((mat_ms + plain_ms) / ms, 3),
+            "unique_kv_mb": round(A.unique_kv_bytes(wp) / 1e6, 2),
+            "logical_kv_mb": round(A.logical_kv_bytes(wp) / 1e6, 2),
+        },
+    }
+    del k_mat
+
+    # ---------------- decode ----------------
+    if not args.no_decode:
+        log("decode workload: generating")
+        wd = W.rag_decode(seed=2)
+        dd = ops.upload(wd, dev)
+        cfgd = dd.cfg
+        dbytes = A.algorithmic_bytes(wd)
+        wsd_bytes = ops.decode_workspace_size(cfgd, wd.batch, wd.max_kv_len)
+        wsd = torch.empty(max(wsd_bytes, 16), dtype=torch.uint8, device=dev)
+        outd = torch.empty_like(dd.q)
+        lsed = torch.empty((wd.batch, wd.num_q_heads), dtype=torch.float32, device=dev)
+        log("decode: timing")
+        dms = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
+                                       wd.max_kv_len, out=outd, lse=lsed, workspace=wsd), args.steps, args.warmup)
+        dnorot = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
+                                          wd.max_kv_len, out=outd, lse=lsed, workspace=wsd, plain=True),
+                       args.steps, args.warmup)
+        tkv = int(wd.chunks["len"].astype(np.int64).sum())
+        kmd = torch.empty(cfgd.num_kv_heads * tkv * cfgd.head_dim, dtype=torch.bfloat16, device=dev)
+        chd = torch.empty_like(dd.chunks)
+        mxc = int(wd.chunks["len"].max())
+        dmat = timed(lambda: ops.materialize_k(cfgd, dd.pool, dd.chunks, mxc, tkv, k_out=kmd, chunks_out=chd),
+                     max(5, args.steps // 5), 2)
+        dplain = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, kmd, dd.pool, chd, dd.chunk_start, wd.max_kv_len,
+                                          out=outd, lse=lsed, workspace=wsd, plain=True), args.steps, args.warmup)
+        gbps = dbytes / (dms * 1e-3) / 1e9
+        result["decode"] = {
+            "workload": "rag_decode: batch 64, 32/8 heads, head_dim 128, 16 x 1024-token chunks from a 256-chunk "
+                        "pool + 65-token private tail, one query per request",
+            "ms": round(dms, 5),
+            "logical_hbm_gbps": round(gbps, 1),
+            "hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
+            "logical_mb": round(dbytes / 1e6, 1),
+            "unique_kv_mb": round(A.unique_kv_bytes(wd) / 1e6, 1),
+            "splits": int(wsd_bytes // (wd.batch * wd.num_q_heads * (wd.head_dim + 2) * 4)) if wsd_bytes else 1,
+            "no_rotation_ms": round(dnorot, 5),
+            "rotation_overhead": round(dms / dnorot - 1.0, 4),
+            "materialize_ms": round(dmat, 5),
+            "plain_decode_ms": round(dplain, 5),
+            "materialize_then_attend_ms": round(dmat + dplain, 5),
+            "speedup_vs_materialize": round((dmat + dplain) / dms, 3),
+        }
+        del kmd, dd
+
+    if args.copy_probe_mib > 0:
+        n = args.copy_probe_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_probe_bytes"] = n * 4
+
+    if not args.no_cpu and rank == 0:
+        log("cpu baseline: timing the oracle")
+        result["cpu_baseline"] = cpu_baseline(wp, flops)
+
+    if rank == 0:
+        print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
