@@ -14,7 +14,8 @@
 // Rotation angles are stateless (Appendix "Long-Context Scalability and Numerical Stability": absolute indices,
 // no recurrence).  theta_t is held in revolutions per position in fp64; for a tile whose row 0 sits at position b
 // the workgroup computes cos/sin(b theta_t) once per t, and each loader thread keeps cos/sin(delta theta_t) for
-// its fixed row delta in registers; the angle of row b + delta follows by one angle addition.
+// its fixed row delta in a private slice of LDS (written once per workgroup); the angle of row b + delta follows by
+// one angle addition.
 //
 // Operand layouts (verified for v_mfma_f32_32x32x16_bf16 and v_mfma_f32_16x16x32_bf16):
 //   32x32x16: A[i][k] in lane i%32 ... k = 8*(lane/32)+e; B[k][j] in lane j%32, k = 8*(lane/32)+e;
@@ -48,6 +49,9 @@ constexpr int kThreads = 256;
 constexpr int kSub = 64;  // keys of one loader sub-tile; tile row 0 of a sub-tile is a multiple of 64 in its chunk
 constexpr int kPad = 8;   // bf16 elements of padding per LDS row
 constexpr float kLn2 = 0.69314718055994530942f;
+// The softmax reference max only moves when a tile's max exceeds it by more than this (log2 units): unnormalised
+// probabilities stay below 2^8, far inside fp32 and bf16 range, and the O accumulator is rescaled rarely.
+constexpr float kRescaleSlack = 8.0f;
 constexpr double kInvTwoPi = 0.15915494309189533577;
 
 static_assert(kPrefillTileKeys == kSub, "prefill tiles are one loader sub-tile");
@@ -159,18 +163,38 @@ struct TileIter {
   }
 };
 
+// LDS of one workgroup.  Bank-conflict notes (64 lanes, 4-byte banks; a 16-byte access pattern is conflict free
+// when every group of 8 consecutive lanes covers distinct 16-byte bank groups):
+//  - K tile rows are D + 8 elements apart (a 4-bank shift per row); the 16-byte blocks of a row are permuted by
+//    kblk() so that the four loader threads writing one row do not collide.
+//  - V^T tile rows are KEYS + 8 elements apart; 16-byte key blocks are XOR-swizzled with (row / 8), otherwise the
+//    transposing writes of rows 8 apart (one per dimension group) would all land in one bank.
+//  - cos/sin tables interleave (c, s) and leave 8 floats of gap per loader quarter and a 4-float row tail so that
+//    the 16-byte reads of the threads of one 8-lane group hit distinct banks.
 template <int D, int NSUB>
 struct Smem {
   static constexpr int KEYS = kSub * NSUB;
-  static constexpr int KLD = D + kPad;     // K tile: [KEYS][KLD], head dimension in virtual order
-  static constexpr int VLD = KEYS + kPad;  // V^T tile: [D][VLD], keys permuted within groups of 16
+  static constexpr int KLD = D + kPad;       // K tile: [KEYS][KLD], head dimension in virtual order
+  static constexpr int VLD = KEYS + kPad;    // V^T tile: [D][VLD], keys permuted within groups of 16
+  static constexpr int VNB = KEYS / 8;       // 16-byte key blocks per V^T row
+  static constexpr int PP = D / 8;           // rotation pairs per loader thread
+  static constexpr int CSW = D + 32;         // floats per cos/sin row: (c, s) of pair t at 2t + 8 * (t / PP)
+  static constexpr int CSD_LD = CSW + 4;     // row stride of the per-row table (4 banks of shift per row)
   uint16_t k[KEYS * KLD] __attribute__((aligned(16)));
   uint16_t vt[D * VLD] __attribute__((aligned(16)));
-  float2 cs[NSUB][D / 2];                  // cos/sin(b_s theta_t) of the current tile's sub-tile bases
-  double freq[D / 2];                      // theta_t / 2pi
+  float csd[kSub * CSD_LD] __attribute__((aligned(16)));  // cos/sin(delta theta_t) for tile rows delta < 64
+  float csb[NSUB][CSW] __attribute__((aligned(16)));      // cos/sin(b_s theta_t) of the current sub-tile bases
+  double freq[D / 2];                                     // theta_t / 2pi
 };
 
 __device__ __forceinline__ int perm4(int x) { return ((x & 1) << 1) | ((x >> 1) & 1); }
+// Physical position of 16-byte block b of a K tile row.
+__device__ __forceinline__ int kblk(int b) { return b ^ (((b >> 3) & 1) << 1); }
+// Element offset of the 16-byte key block b of V^T row r.
+template <int VNB>
+__device__ __forceinline__ int vt_off(int r, int b) { return 8 * (b ^ ((r >> 3) & (VNB - 1))); }
+template <int D>
+__device__ __forceinline__ int cs_idx(int t) { return 2 * t + 8 * (t / (D / 8)); }
 
 // Cooperative tile loader: 256 threads bring NSUB sub-tiles of 64 keys into LDS, rotating K if ROT.
 // K: thread = (row = tid/4, quarter = tid%4) handles pairs t in [quarter*D/8, (quarter+1)*D/8).
@@ -183,44 +207,66 @@ struct Loader {
   using S = Smem<D, NSUB>;
   u32x4 klo[NSUB][NV], khi[NSUB][NV];
   u32x4 vr[NSUB][4];
-  float2 csd[ROT ? PP : 1];
   int tid, row, quarter, vdg, va;
 
-  __device__ void init(int t, const double* freq) {
+  // Per-row angle table: written once per workgroup (visible after the caller's next barrier).
+  __device__ void init(int t, S& sm) {
     tid = t;
     row = t >> 2;
     quarter = t & 3;
     vdg = t % (D / 8);
     va = t / (D / 8);
     if (ROT) {
+      float* cd = sm.csd + row * S::CSD_LD;
 #pragma unroll
-      for (int e = 0; e < PP; ++e) csd[e] = rope_cs(row, freq[quarter * PP + e]);
+      for (int e = 0; e < PP; ++e) {
+        const int tt = quarter * PP + e;
+        *reinterpret_cast<float2*>(cd + cs_idx<D>(tt)) = rope_cs(row, sm.freq[tt]);
+      }
     }
   }
 
-  // Global loads of one tile: kbase / vbase = K / V of this head at the tile's first key.
+  // Global loads of one tile: kbase / vbase = K / V of this head at the tile's first key (nvalid >= 1 rows).
+  // Rows past the chunk's end read row 0 instead and are zeroed: straight-line code keeps the prefetch buffers in
+  // registers.
   __device__ void fetch(const uint16_t* kbase, const uint16_t* vbase, int nvalid) {
+    const u32x4 zero = {0, 0, 0, 0};
+    if (nvalid >= NSUB * kSub) {
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) {
+        const uint16_t* src = kbase + (size_t)(s * kSub + row) * D + quarter * PP;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          klo[s][v] = reinterpret_cast<const u32x4*>(src)[v];
+          khi[s][v] = reinterpret_cast<const u32x4*>(src + D / 2)[v];
+        }
+        if (tid < VTASKS) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            vr[s][i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)(s * kSub + 4 * va + i) * D + 8 * vdg);
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) {
       const int r = s * kSub + row;
-      if (r < nvalid) {
-        const u32x4* lo = reinterpret_cast<const u32x4*>(kbase + (size_t)r * D + quarter * PP);
-        const u32x4* hi = reinterpret_cast<const u32x4*>(kbase + (size_t)r * D + D / 2 + quarter * PP);
+      const bool ok = r < nvalid;
+      const uint16_t* src = kbase + (size_t)(ok ? r : 0) * D + quarter * PP;
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          klo[s][v] = lo[v];
-          khi[s][v] = hi[v];
-        }
-      } else {
-#pragma unroll
-        for (int v = 0; v < NV; ++v) klo[s][v] = khi[s][v] = u32x4{0, 0, 0, 0};
+      for (int v = 0; v < NV; ++v) {
+        const u32x4 lo = reinterpret_cast<const u32x4*>(src)[v];
+        const u32x4 hi = reinterpret_cast<const u32x4*>(src + D / 2)[v];
+        klo[s][v] = ok ? lo : zero;
+        khi[s][v] = ok ? hi : zero;
       }
       if (tid < VTASKS) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int rr = s * kSub + 4 * va + i;
-          vr[s][i] = rr < nvalid ? *reinterpret_cast<const u32x4*>(vbase + (size_t)rr * D + 8 * vdg)
-                                 : u32x4{0, 0, 0, 0};
+          const bool vok = rr < nvalid;
+          const u32x4 x = *reinterpret_cast<const u32x4*>(vbase + (size_t)(vok ? rr : 0) * D + 8 * vdg);
+          vr[s][i] = vok ? x : zero;
         }
       }
     }
@@ -230,6 +276,8 @@ struct Loader {
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) {
       uint16_t* krow = sm.k + (s * kSub + row) * S::KLD;
+      const float* cb = sm.csb[s];
+      const float* cd = sm.csd + row * S::CSD_LD;
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
         const int t0 = quarter * PP + 8 * v;  // first pair of this 8-pair group
@@ -241,7 +289,9 @@ struct Loader {
             const uint32_t wl = klo[s][v][e >> 1], wh = khi[s][v][e >> 1];
             const float x1 = (e & 1) ? bf_hi(wl) : bf_lo(wl);
             const float x2 = (e & 1) ? bf_hi(wh) : bf_lo(wh);
-            rotate_pair(x1, x2, sm.cs[s][t0 + e], csd[8 * v + e], yl[e], yh[e]);
+            const int ci = cs_idx<D>(t0 + e);
+            rotate_pair(x1, x2, *reinterpret_cast<const float2*>(cb + ci), *reinterpret_cast<const float2*>(cd + ci),
+                        yl[e], yh[e]);
           }
           w0 = u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yh[0], yh[1]), pack2(yh[2], yh[3])};
           w1 = u32x4{pack2(yl[4], yl[5]), pack2(yl[6], yl[7]), pack2(yh[4], yh[5]), pack2(yh[6], yh[7])};
@@ -249,8 +299,8 @@ struct Loader {
           w0 = u32x4{klo[s][v][0], klo[s][v][1], khi[s][v][0], khi[s][v][1]};
           w1 = u32x4{klo[s][v][2], klo[s][v][3], khi[s][v][2], khi[s][v][3]};
         }
-        *reinterpret_cast<u32x4*>(krow + 2 * t0) = w0;
-        *reinterpret_cast<u32x4*>(krow + 2 * t0 + 8) = w1;
+        *reinterpret_cast<u32x4*>(krow + 8 * kblk(t0 / 4)) = w0;
+        *reinterpret_cast<u32x4*>(krow + 8 * kblk(t0 / 4 + 1)) = w1;
       }
       if (tid < VTASKS) {
         const int kk = s * kSub + 4 * va;
@@ -261,8 +311,9 @@ struct Loader {
                              __builtin_amdgcn_perm(vr[s][3][w], vr[s][2][w], 0x05040100u)};
           const u32x2 hi2 = {__builtin_amdgcn_perm(vr[s][1][w], vr[s][0][w], 0x07060302u),
                              __builtin_amdgcn_perm(vr[s][3][w], vr[s][2][w], 0x07060302u)};
-          *reinterpret_cast<u32x2*>(sm.vt + (8 * vdg + 2 * w) * S::VLD + col) = lo2;
-          *reinterpret_cast<u32x2*>(sm.vt + (8 * vdg + 2 * w + 1) * S::VLD + col) = hi2;
+          const int r0 = 8 * vdg + 2 * w, r1 = r0 + 1;
+          *reinterpret_cast<u32x2*>(sm.vt + r0 * S::VLD + vt_off<S::VNB>(r0, col >> 3) + (col & 7)) = lo2;
+          *reinterpret_cast<u32x2*>(sm.vt + r1 * S::VLD + vt_off<S::VNB>(r1, col >> 3) + (col & 7)) = hi2;
         }
       }
     }
@@ -273,7 +324,7 @@ template <int D, int NSUB>
 __device__ __forceinline__ void compute_base(Smem<D, NSUB>& sm, int tid, int b0) {
   for (int e = tid; e < NSUB * (D / 2); e += kThreads) {
     const int s = e / (D / 2), t = e % (D / 2);
-    sm.cs[s][t] = rope_cs(b0 + s * kSub, sm.freq[t]);
+    *reinterpret_cast<float2*>(sm.csb[s] + cs_idx<D>(t)) = rope_cs(b0 + s * kSub, sm.freq[t]);
   }
 }
 
@@ -305,17 +356,32 @@ __device__ __forceinline__ const uint16_t* v_ptr(const uint16_t* pool, const Rec
 // Prefill: workgroup = (row tile of 128 packed query rows, KV head, request x split).  Packed row = token * G + g
 // (the G query heads sharing one KV head, Sec. 3.5), four waves x 32 rows, one row per lane pair (lane, lane+32).
 // ---------------------------------------------------------------------------------------------------------------
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).  Remapping the linear workgroup id
+// so that consecutive logical ids share an XCD puts the row tiles that read the same keys onto one L2.
+__device__ __forceinline__ int xcd_remap(int id, int n) {
+  const int per = n >> 3;
+  return id < (per << 3) ? (id & 7) * per + (id >> 3) : id;
+}
+
 template <int D, bool ROT>
-__global__ __launch_bounds__(kThreads) void prefill_kernel(AttnArgs a) {
+#ifndef LAZY_PREFILL_WAVES_PER_EU
+#define LAZY_PREFILL_WAVES_PER_EU 2
+#endif
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(LAZY_PREFILL_WAVES_PER_EU, LAZY_PREFILL_WAVES_PER_EU))) void prefill_kernel(AttnArgs a) {
   __shared__ Smem<D, 1> sm;
   using S = Smem<D, 1>;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g = blockIdx.y;
-  const int r = blockIdx.z / a.splits, split = blockIdx.z % a.splits;
+  const int nx = gridDim.x, ny = gridDim.y;
+  const int lid = xcd_remap(blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z), nx * ny * gridDim.z);
+  const int qtile = lid % nx;
+  const int g = (lid / nx) % ny;
+  const int zz = lid / (nx * ny);
+  const int r = zz / a.splits, split = zz % a.splits;
   const int qs = a.q_start[r], qe = a.q_start[r + 1];
   const int G = a.group;
   const int nrows = (qe - qs) * G;
-  const int row0 = blockIdx.x * kPrefillRows;
+  const int row0 = qtile * kPrefillRows;
   if (row0 >= nrows) return;
   const int qp0 = a.q_pos0[r];
 
@@ -345,7 +411,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnArgs a) {
   const float c = a.scale_log2;
 
   Loader<D, 1, ROT> ld;
-  ld.init(tid, sm.freq);
+  ld.init(tid, sm);
   TileIter<kSub> it;
   it.init(a.chunks, a.chunk_start[r], a.chunk_start[r + 1], split, a.splits);
   bool have = it.seek(a.causal, qmax);
@@ -370,7 +436,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnArgs a) {
     for (int s = 0; s < D / 16; ++s) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(sm.k + (32 * blk + (lane & 31)) * S::KLD + 16 * s + 8 * h2);
+        const u32x4 kv =
+            *reinterpret_cast<const u32x4*>(sm.k + (32 * blk + (lane & 31)) * S::KLD + 8 * kblk(2 * s + h2));
         sa[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[s], sa[blk], 0, 0, 0);
       }
     }
@@ -390,9 +457,18 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sa[blk][i]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(m2, mx * c);
-    const float muse = mnew == -INFINITY ? 0.f : mnew;
-    const float alpha = fast_exp2(m2 - muse);
+    // Lazy rescale: the running reference max m2 only moves when this tile's max exceeds it by more than
+    // kRescaleSlack (log2 units), so probabilities stay below 2^kRescaleSlack and O is rarely touched.
+    const float mt = mx * c;
+    if (__any(mt > m2 + kRescaleSlack)) {
+      const float mnew = fmaxf(m2, mt);
+      const float alpha = m2 == -INFINITY ? 0.f : fast_exp2(m2 - mnew);
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) o[db] *= alpha;
+      m2 = mnew;
+    }
+    const float muse = m2 == -INFINITY ? 0.f : m2;
     float ps = 0.f;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
@@ -402,10 +478,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnArgs a) {
         sa[blk][i] = p;
         ps += p;
       }
-    lsum = fmaf(lsum, alpha, ps);
-    m2 = mnew;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) o[db] *= alpha;
+    lsum += ps;
 
     // O^T += V^T P^T: four 16-key steps.
 #pragma unroll
@@ -416,8 +489,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnArgs a) {
                                         pack2(sv[b + 4], sv[b + 5]), pack2(sv[b + 6], sv[b + 7])});
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        const u32x4 vv =
-            *reinterpret_cast<const u32x4*>(sm.vt + (32 * db + (lane & 31)) * S::VLD + 16 * s2 + 8 * h2);
+        const int vrow = 32 * db + (lane & 31);
+        const u32x4 vv = *reinterpret_cast<const u32x4*>(sm.vt + vrow * S::VLD + vt_off<S::VNB>(vrow, 2 * s2 + h2));
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pb, o[db], 0, 0, 0);
       }
     }
@@ -500,7 +573,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
   const float c = a.scale_log2;
 
   Loader<D, 2, ROT> ld;
-  ld.init(tid, sm.freq);
+  ld.init(tid, sm);
   TileIter<2 * kSub> it;
   it.init(a.chunks, a.chunk_start[r], a.chunk_start[r + 1], split, a.splits);
   bool have = it.seek(a.causal, qpos);
@@ -525,7 +598,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
         const int key = 32 * wave + kappa(b, col);
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(sm.k + key * S::KLD + 32 * s + 8 * kq);
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(sm.k + key * S::KLD + 8 * kblk(4 * s + kq));
         sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kv), qf[s], sa[b], 0, 0, 0);
       }
     }
@@ -546,9 +619,16 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
       for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sa[b][i]);
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(m2, mx * c);
-    const float muse = mnew == -INFINITY ? 0.f : mnew;
-    const float alpha = fast_exp2(m2 - muse);
+    const float mt = mx * c;
+    if (__any(mt > m2 + kRescaleSlack)) {
+      const float mnew = fmaxf(m2, mt);
+      const float alpha = m2 == -INFINITY ? 0.f : fast_exp2(m2 - mnew);
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db) o[db] *= alpha;
+      m2 = mnew;
+    }
+    const float muse = m2 == -INFINITY ? 0.f : m2;
     float ps = 0.f;
 #pragma unroll
     for (int b = 0; b < 2; ++b)
@@ -558,14 +638,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
         sa[b][i] = p;
         ps += p;
       }
-    lsum = fmaf(lsum, alpha, ps);
-    m2 = mnew;
+    lsum += ps;
     const bf16x8 pb = as_bf16x8(u32x4{pack2(sa[0][0], sa[0][1]), pack2(sa[0][2], sa[0][3]),
                                       pack2(sa[1][0], sa[1][1]), pack2(sa[1][2], sa[1][3])});
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) {
-      o[db] *= alpha;
-      const u32x4 vv = *reinterpret_cast<const u32x4*>(sm.vt + (16 * db + col) * S::VLD + 32 * wave + 8 * kq);
+      const int vrow = 16 * db + col;
+      const u32x4 vv = *reinterpret_cast<const u32x4*>(sm.vt + vrow * S::VLD + vt_off<S::VNB>(vrow, 4 * wave + kq));
       o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vv), pb, o[db], 0, 0, 0);
     }
     have = have_next;
