@@ -9,6 +9,7 @@
 
 namespace {
 
+constexpr int kNumCUs = 256;              // MI355X compute units
 constexpr int kTargetWorkgroups = 1024;  // 256 CUs x ~4 resident workgroups
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -29,16 +30,25 @@ float scale_log2(const lazy_attn_params_t* p) {
   return s * 1.4426950408889634f;
 }
 
+// 256 packed rows per workgroup (eight waves, one workgroup per CU; head_dim 128 only) once a request has enough
+// rows; otherwise 128 rows (four waves, two workgroups per CU).  Must match the kernel chosen in launch_prefill.
+int prefill_row_blocks(const lazy_attn_params_t* p, int32_t max_q_len) {
+  const int64_t g = p->num_q_heads / p->num_kv_heads;
+  return p->head_dim == 128 && (int64_t)max_q_len * g >= 2 * lazy::kPrefillRowsPerBlock ? 2 : 1;
+}
+
 int prefill_q_tiles(const lazy_attn_params_t* p, int32_t max_q_len) {
   const int64_t g = p->num_q_heads / p->num_kv_heads;
-  return (int)ceil_div((int64_t)max_q_len * g, lazy::kPrefillRows);
+  return (int)ceil_div((int64_t)max_q_len * g, (int64_t)lazy::kPrefillRowsPerBlock * prefill_row_blocks(p, max_q_len));
 }
 
 int prefill_splits(const lazy_attn_params_t* p, int32_t batch, int32_t max_q_len, int32_t max_kv_len) {
   if (p->num_splits > 0) return p->num_splits;
   const int64_t base = (int64_t)prefill_q_tiles(p, max_q_len) * p->num_kv_heads * batch;
   const int64_t tiles = ceil_div(max_kv_len, lazy::kPrefillTileKeys);
-  int64_t s = base > 0 ? ceil_div(kTargetWorkgroups, base) : 1;
+  // 256-row workgroups occupy a whole CU (LDS), 128-row ones leave room for two per CU.
+  const int64_t target = prefill_row_blocks(p, max_q_len) == 2 ? kNumCUs : 2 * kNumCUs;
+  int64_t s = base > 0 ? ceil_div(target, base) : 1;
   const int64_t cap = tiles / 4 > 1 ? tiles / 4 : 1;  // keep at least ~4 key tiles per split
   if (s > cap) s = cap;
   if (s > 64) s = 64;
@@ -106,6 +116,7 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
   a.causal = p->causal;
   a.splits = splits;
   a.q_tiles = q_tiles;
+  a.row_blocks = prefill_row_blocks(p, max_q_len);
   a.head_groups = 1;
   a.rope_base = p->rope_base;
   a.scale_log2 = scale_log2(p);
@@ -148,6 +159,7 @@ int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const 
   a.causal = p->causal;
   a.splits = splits;
   a.q_tiles = 1;
+  a.row_blocks = 1;
   a.head_groups = hg;
   a.rope_base = p->rope_base;
   a.scale_log2 = scale_log2(p);

@@ -30,13 +30,14 @@ struct AttnArgs {
   int32_t causal;
   int32_t splits;
   int32_t q_tiles;            // prefill: row tiles per (request, kv head)
+  int32_t row_blocks;         // prefill: a workgroup covers 128 * row_blocks packed rows (2 = eight-wave kernel)
   int32_t head_groups;        // decode: ceil(group / 16)
   float rope_base;
   float scale_log2;           // softmax scale * log2(e)
 };
 
 // Packed rows (token, head in group) handled by one prefill workgroup, and keys per decode tile.
-constexpr int kPrefillRows = 128;
+constexpr int kPrefillRowsPerBlock = 128;  // packed rows of a prefill workgroup per row block
 constexpr int kPrefillTileKeys = 64;
 constexpr int kDecodeTileKeys = 128;
 constexpr int kDecodeHeadsPerGroup = 16;

@@ -6,7 +6,7 @@
 //
 // Data path of one key tile (64 keys per sub-tile, shared by the four waves of a workgroup):
 //   global K rows (bf16, natural layout) --16 B loads--> registers --fp32 rotation--> bf16 --> LDS K tile
-//   global V rows --16 B loads--> registers --4x8 transpose (v_perm)--> LDS V^T tile
+//   global V rows --16 B loads--> registers --> LDS V tile (row-major), read back transposed by ds_read_b64_tr_b16
 // The rotation is done once per workgroup and tile (not once per wave), which matters on gfx950 where the bf16
 // MFMA rate is 16x the fp32 VALU rate: the relative cost of rotating K is 3/(4M) in FLOPs (eq. prefilling) but
 // paid at VALU speed.
@@ -26,8 +26,8 @@
 // The head dimension inside the K tile and in the Q fragments is stored in a permuted "virtual" order that puts
 // each rotation pair (t, t + D/2) into the same 16-byte group: for pair t, the low half goes to virtual column
 // 16*(t/8) + 8*((t%8)/4) + t%4 and the high half four columns later.  Any permutation applied to both Q and K
-// leaves Q K^T unchanged.  The key axis of the V^T tile is permuted inside each group of 16 keys
-// (0-3, 8-11, 4-7, 12-15) so that P leaves the S^T accumulators directly in the B-operand order.
+// leaves Q K^T unchanged.  V fragments are gathered with transposing LDS reads whose rows follow the key order
+// in which P leaves the S^T accumulators, so P needs no shuffling.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -104,7 +104,16 @@ struct Rec {
   int len, pos, kst, vst;
 };
 
-__device__ __forceinline__ Rec load_rec(const lazy_chunk_t* c) {
+// Read-only tables are read through the constant address space: uniform loads from it become scalar loads, whose
+// waits (lgkmcnt) do not drain the vector-memory queue that holds the next tile's prefetched K / V.
+template <typename T>
+using cptr = const T __attribute__((address_space(4)))*;
+template <typename T>
+__device__ __forceinline__ cptr<T> as_const(const T* p) {
+  return (cptr<T>)p;
+}
+
+__device__ __forceinline__ Rec load_rec(cptr<lazy_chunk_t> c) {
   Rec r;
   r.koff = c->k_offset;
   r.voff = c->v_offset;
@@ -120,11 +129,12 @@ __device__ __forceinline__ Rec load_rec(const lazy_chunk_t* c) {
 // evenly.  With the causal rule, tiles whose first key lies after the last query of the workgroup are skipped.
 template <int TK>
 struct TileIter {
-  const lazy_chunk_t* recs;
+  cptr<lazy_chunk_t> recs;
   int i, end, j0, left;
   Rec cur;
 
-  __device__ void init(const lazy_chunk_t* chunks, int c0, int c1, int split, int splits) {
+  __device__ void init(const lazy_chunk_t* table, int c0, int c1, int split, int splits) {
+    const cptr<lazy_chunk_t> chunks = as_const(table);
     recs = chunks;
     end = c1;
     int ntiles = 0;
@@ -167,32 +177,37 @@ struct TileIter {
 // when every group of 8 consecutive lanes covers distinct 16-byte bank groups):
 //  - K tile rows are D + 8 elements apart (a 4-bank shift per row); the 16-byte blocks of a row are permuted by
 //    kblk() so that the four loader threads writing one row do not collide.
-//  - V^T tile rows are KEYS + 8 elements apart; 16-byte key blocks are XOR-swizzled with (row / 8), otherwise the
-//    transposing writes of rows 8 apart (one per dimension group) would all land in one bank.
+//  - The V tile is row-major (key, dimension) with rows D + 16 elements apart: the 16-byte writes of a row are
+//    contiguous, and the transposing reads (ds_read_b64_tr_b16: 16 lanes read 4 rows x 32 bytes) hit 4 disjoint
+//    8-bank groups.
 //  - cos/sin tables interleave (c, s) and leave 8 floats of gap per loader quarter and a 4-float row tail so that
 //    the 16-byte reads of the threads of one 8-lane group hit distinct banks.
 template <int D, int NSUB>
 struct Smem {
   static constexpr int KEYS = kSub * NSUB;
   static constexpr int KLD = D + kPad;       // K tile: [KEYS][KLD], head dimension in virtual order
-  static constexpr int VLD = KEYS + kPad;    // V^T tile: [D][VLD], keys permuted within groups of 16
-  static constexpr int VNB = KEYS / 8;       // 16-byte key blocks per V^T row
+  static constexpr int VLD = D + 16;         // V tile: [KEYS][VLD], natural layout
   static constexpr int PP = D / 8;           // rotation pairs per loader thread
   static constexpr int CSW = D + 32;         // floats per cos/sin row: (c, s) of pair t at 2t + 8 * (t / PP)
   static constexpr int CSD_LD = CSW + 4;     // row stride of the per-row table (4 banks of shift per row)
   uint16_t k[KEYS * KLD] __attribute__((aligned(16)));
-  uint16_t vt[D * VLD] __attribute__((aligned(16)));
+  uint16_t v[KEYS * VLD] __attribute__((aligned(16)));
   float csd[kSub * CSD_LD] __attribute__((aligned(16)));  // cos/sin(delta theta_t) for tile rows delta < 64
   float csb[NSUB][CSW] __attribute__((aligned(16)));      // cos/sin(b_s theta_t) of the current sub-tile bases
   double freq[D / 2];                                     // theta_t / 2pi
 };
 
-__device__ __forceinline__ int perm4(int x) { return ((x & 1) << 1) | ((x >> 1) & 1); }
 // Physical position of 16-byte block b of a K tile row.
 __device__ __forceinline__ int kblk(int b) { return b ^ (((b >> 3) & 1) << 1); }
-// Element offset of the 16-byte key block b of V^T row r.
-template <int VNB>
-__device__ __forceinline__ int vt_off(int r, int b) { return 8 * (b ^ ((r >> 3) & (VNB - 1))); }
+// Transposing LDS read (gfx950 ds_read_b64_tr_b16).  Within each group of 16 lanes, lane i supplies the address
+// of 4 consecutive 16-bit elements M[i][0..3]; lane j receives M[4e + j/4][j%4] for e = 0..3.  With lane i pointing
+// at row (base + i/4) and column (4 * (i%4)) of a row-major tile, lane j gets column j of rows base..base+3, which is
+// an MFMA operand fragment of four consecutive keys for one dimension.
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x2 tr_read(const uint16_t* p) {
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
+}
 template <int D>
 __device__ __forceinline__ int cs_idx(int t) { return 2 * t + 8 * (t / (D / 8)); }
 
@@ -203,19 +218,17 @@ template <int D, int NSUB, bool ROT>
 struct Loader {
   static constexpr int PP = D / 8;
   static constexpr int NV = PP / 8;
-  static constexpr int VTASKS = (kSub / 4) * (D / 8);
+  static constexpr int VC = kSub * (D / 8) / kThreads;  // 16-byte V chunks per thread and sub-tile
   using S = Smem<D, NSUB>;
   u32x4 klo[NSUB][NV], khi[NSUB][NV];
-  u32x4 vr[NSUB][4];
-  int tid, row, quarter, vdg, va;
+  u32x4 vr[NSUB][VC];
+  int tid, row, quarter;
 
   // Per-row angle table: written once per workgroup (visible after the caller's next barrier).
   __device__ void init(int t, S& sm) {
     tid = t;
     row = t >> 2;
     quarter = t & 3;
-    vdg = t % (D / 8);
-    va = t / (D / 8);
     if (ROT) {
       float* cd = sm.csd + row * S::CSD_LD;
 #pragma unroll
@@ -240,10 +253,10 @@ struct Loader {
           klo[s][v] = reinterpret_cast<const u32x4*>(src)[v];
           khi[s][v] = reinterpret_cast<const u32x4*>(src + D / 2)[v];
         }
-        if (tid < VTASKS) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            vr[s][i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)(s * kSub + 4 * va + i) * D + 8 * vdg);
+        for (int i = 0; i < VC; ++i) {
+          const int c = tid + kThreads * i;
+          vr[s][i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)(s * kSub + c / (D / 8)) * D + 8 * (c % (D / 8)));
         }
       }
       return;
@@ -260,14 +273,13 @@ struct Loader {
         klo[s][v] = ok ? lo : zero;
         khi[s][v] = ok ? hi : zero;
       }
-      if (tid < VTASKS) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int rr = s * kSub + 4 * va + i;
-          const bool vok = rr < nvalid;
-          const u32x4 x = *reinterpret_cast<const u32x4*>(vbase + (size_t)(vok ? rr : 0) * D + 8 * vdg);
-          vr[s][i] = vok ? x : zero;
-        }
+      for (int i = 0; i < VC; ++i) {
+        const int c = tid + kThreads * i;
+        const int rr = s * kSub + c / (D / 8);
+        const bool vok = rr < nvalid;
+        const u32x4 x = *reinterpret_cast<const u32x4*>(vbase + (size_t)(vok ? rr : 0) * D + 8 * (c % (D / 8)));
+        vr[s][i] = vok ? x : zero;
       }
     }
   }
@@ -302,19 +314,10 @@ struct Loader {
         *reinterpret_cast<u32x4*>(krow + 8 * kblk(t0 / 4)) = w0;
         *reinterpret_cast<u32x4*>(krow + 8 * kblk(t0 / 4 + 1)) = w1;
       }
-      if (tid < VTASKS) {
-        const int kk = s * kSub + 4 * va;
-        const int col = (kk & ~15) + 4 * perm4((kk >> 2) & 3);
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const u32x2 lo2 = {__builtin_amdgcn_perm(vr[s][1][w], vr[s][0][w], 0x05040100u),
-                             __builtin_amdgcn_perm(vr[s][3][w], vr[s][2][w], 0x05040100u)};
-          const u32x2 hi2 = {__builtin_amdgcn_perm(vr[s][1][w], vr[s][0][w], 0x07060302u),
-                             __builtin_amdgcn_perm(vr[s][3][w], vr[s][2][w], 0x07060302u)};
-          const int r0 = 8 * vdg + 2 * w, r1 = r0 + 1;
-          *reinterpret_cast<u32x2*>(sm.vt + r0 * S::VLD + vt_off<S::VNB>(r0, col >> 3) + (col & 7)) = lo2;
-          *reinterpret_cast<u32x2*>(sm.vt + r1 * S::VLD + vt_off<S::VNB>(r1, col >> 3) + (col & 7)) = hi2;
-        }
+      for (int i = 0; i < VC; ++i) {
+        const int c = tid + kThreads * i;
+        *reinterpret_cast<u32x4*>(sm.v + (s * kSub + c / (D / 8)) * S::VLD + 8 * (c % (D / 8))) = vr[s][i];
       }
     }
   }
@@ -353,8 +356,12 @@ __device__ __forceinline__ const uint16_t* v_ptr(const uint16_t* pool, const Rec
 }
 
 // ---------------------------------------------------------------------------------------------------------------
-// Prefill: workgroup = (row tile of 128 packed query rows, KV head, request x split).  Packed row = token * G + g
-// (the G query heads sharing one KV head, Sec. 3.5), four waves x 32 rows, one row per lane pair (lane, lane+32).
+// Prefill: workgroup = (row tile of 128*RB packed query rows, KV head, request x split).  Packed row = token * G + g
+// (the G query heads sharing one KV head, Sec. 3.5).  Four waves; each wave owns RB blocks of 32 rows, one row per
+// lane pair (lane, lane+32).  With RB = 2 every K / V fragment read from LDS feeds two MFMAs and the K rotation of
+// a tile is shared by 256 rows.  NBUF = 2 double-buffers the LDS tiles (one barrier per tile, the next tile's
+// global loads in flight during the current tile's MFMAs); NBUF = 1 keeps the LDS small enough for two
+// workgroups per CU.
 // ---------------------------------------------------------------------------------------------------------------
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).  Remapping the linear workgroup id
 // so that consecutive logical ids share an XCD puts the row tiles that read the same keys onto one L2.
@@ -363,14 +370,139 @@ __device__ __forceinline__ int xcd_remap(int id, int n) {
   return id < (per << 3) ? (id & 7) * per + (id >> 3) : id;
 }
 
-template <int D, bool ROT>
-#ifndef LAZY_PREFILL_WAVES_PER_EU
-#define LAZY_PREFILL_WAVES_PER_EU 2
-#endif
-__global__ __launch_bounds__(kThreads)
-__attribute__((amdgpu_waves_per_eu(LAZY_PREFILL_WAVES_PER_EU, LAZY_PREFILL_WAVES_PER_EU))) void prefill_kernel(AttnArgs a) {
-  __shared__ Smem<D, 1> sm;
+template <int D, int NBUF>
+struct PrefillSmem {
   using S = Smem<D, 1>;
+  uint16_t k[NBUF][kSub * S::KLD] __attribute__((aligned(16)));
+  uint16_t v[NBUF][kSub * S::VLD] __attribute__((aligned(16)));
+  float csd[kSub * S::CSD_LD] __attribute__((aligned(16)));
+  float csb[2][S::CSW] __attribute__((aligned(16)));
+  double freq[D / 2];
+};
+
+// Physical 16-byte block of a K tile row for a loader with TPR threads per row: the TPR threads of one row write
+// blocks 16 pairs apart (TPR = 4) or 8 pairs apart (TPR = 8); both swizzles send them to distinct bank groups.
+template <int TPR>
+__device__ __forceinline__ int kblk_t(int b) {
+  return TPR == 8 ? (b ^ ((b >> 3) & 1)) : (b ^ (((b >> 3) & 1) << 1));
+}
+
+// Cooperative loader of one 64-key tile for the prefill kernel with NT threads: TPR = NT / 64 threads per key row,
+// each rotating PP = D / (2 TPR) pairs; V copied row-major in 16-byte chunks (VC per thread).
+// The per-row cos/sin constants are written to a private LDS slice once per workgroup and read per tile.
+template <int D, bool ROT, int NT, bool CSD_REGS = false>
+struct PLoader {
+  using S = Smem<D, 1>;
+  static constexpr int TPR = NT / kSub;
+  static constexpr int PP = D / (2 * TPR);
+  static constexpr int NV = PP / 8;
+  static constexpr int VC = kSub * (D / 8) / NT;
+  static_assert(PP % 8 == 0, "each loader thread rotates whole groups of 8 pairs");
+  u32x4 klo[NV], khi[NV];
+  u32x4 vr[VC];
+  float2 cdr[CSD_REGS && ROT ? PP : 1];
+  int tid, row, part;
+
+  __device__ void init(int t, float* csd, const double* freq) {
+    tid = t;
+    row = t / TPR;
+    part = t % TPR;
+    if (ROT) {
+      float* cd = csd + row * S::CSD_LD;
+#pragma unroll
+      for (int e = 0; e < PP; ++e) {
+        const int tt = part * PP + e;
+        *reinterpret_cast<float2*>(cd + cs_idx<D>(tt)) = rope_cs(row, freq[tt]);
+      }
+      // Read back once: the loop writes LDS, so these registers cannot be re-derived inside it.
+      if (CSD_REGS) {
+#pragma unroll
+        for (int e = 0; e < PP; ++e) cdr[e] = *reinterpret_cast<const float2*>(cd + cs_idx<D>(part * PP + e));
+      }
+    }
+  }
+
+  __device__ void fetch(const uint16_t* kbase, const uint16_t* vbase, int nvalid) {
+    const u32x4 zero = {0, 0, 0, 0};
+    if (nvalid >= kSub) {
+      const uint16_t* src = kbase + (size_t)row * D + part * PP;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        klo[v] = reinterpret_cast<const u32x4*>(src)[v];
+        khi[v] = reinterpret_cast<const u32x4*>(src + D / 2)[v];
+      }
+#pragma unroll
+      for (int i = 0; i < VC; ++i) {
+        const int c = tid + NT * i;
+        vr[i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)(c / (D / 8)) * D + 8 * (c % (D / 8)));
+      }
+      return;
+    }
+    const bool ok = row < nvalid;
+    const uint16_t* src = kbase + (size_t)(ok ? row : 0) * D + part * PP;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const u32x4 lo = reinterpret_cast<const u32x4*>(src)[v];
+      const u32x4 hi = reinterpret_cast<const u32x4*>(src + D / 2)[v];
+      klo[v] = ok ? lo : zero;
+      khi[v] = ok ? hi : zero;
+    }
+#pragma unroll
+    for (int i = 0; i < VC; ++i) {
+      const int c = tid + NT * i;
+      const int rr = c / (D / 8);
+      const bool vok = rr < nvalid;
+      const u32x4 x = *reinterpret_cast<const u32x4*>(vbase + (size_t)(vok ? rr : 0) * D + 8 * (c % (D / 8)));
+      vr[i] = vok ? x : zero;
+    }
+  }
+
+  __device__ void store(uint16_t* kbuf, uint16_t* vtbuf, const float* cb, const float* csd) {
+    uint16_t* krow = kbuf + row * S::KLD;
+    const float* cd = csd + row * S::CSD_LD;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int t0 = part * PP + 8 * v;
+      u32x4 w0, w1;
+      if (ROT) {
+        float yl[8], yh[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x1 = (e & 1) ? bf_hi(klo[v][e >> 1]) : bf_lo(klo[v][e >> 1]);
+          const float x2 = (e & 1) ? bf_hi(khi[v][e >> 1]) : bf_lo(khi[v][e >> 1]);
+          const int ci = cs_idx<D>(t0 + e);
+          const float2 d = CSD_REGS ? cdr[8 * v + e] : *reinterpret_cast<const float2*>(cd + ci);
+          rotate_pair(x1, x2, *reinterpret_cast<const float2*>(cb + ci), d, yl[e], yh[e]);
+        }
+        w0 = u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yh[0], yh[1]), pack2(yh[2], yh[3])};
+        w1 = u32x4{pack2(yl[4], yl[5]), pack2(yl[6], yl[7]), pack2(yh[4], yh[5]), pack2(yh[6], yh[7])};
+      } else {
+        w0 = u32x4{klo[v][0], klo[v][1], khi[v][0], khi[v][1]};
+        w1 = u32x4{klo[v][2], klo[v][3], khi[v][2], khi[v][3]};
+      }
+      *reinterpret_cast<u32x4*>(krow + 8 * kblk_t<TPR>(t0 / 4)) = w0;
+      *reinterpret_cast<u32x4*>(krow + 8 * kblk_t<TPR>(t0 / 4 + 1)) = w1;
+    }
+#pragma unroll
+    for (int i = 0; i < VC; ++i) {
+      const int c = tid + NT * i;
+      *reinterpret_cast<u32x4*>(vtbuf + (c / (D / 8)) * S::VLD + 8 * (c % (D / 8))) = vr[i];
+    }
+  }
+};
+
+template <int D>
+__device__ __forceinline__ void prefill_base(float* csb, const double* freq, int tid, int b0) {
+  if (tid < D / 2) *reinterpret_cast<float2*>(csb + cs_idx<D>(tid)) = rope_cs(b0, freq[tid]);
+}
+
+template <int D, bool ROT, int NW, int NBUF, int RB>
+__global__ __launch_bounds__(NW * 64)
+__attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void prefill_kernel(AttnArgs a) {
+  __shared__ PrefillSmem<D, NBUF> sm;
+  using S = Smem<D, 1>;
+  constexpr int NT = NW * 64;
+  constexpr int BM = 32 * NW * RB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nx = gridDim.x, ny = gridDim.y;
   const int lid = xcd_remap(blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z), nx * ny * gridDim.z);
@@ -378,155 +510,244 @@ __attribute__((amdgpu_waves_per_eu(LAZY_PREFILL_WAVES_PER_EU, LAZY_PREFILL_WAVES
   const int g = (lid / nx) % ny;
   const int zz = lid / (nx * ny);
   const int r = zz / a.splits, split = zz % a.splits;
-  const int qs = a.q_start[r], qe = a.q_start[r + 1];
+  const int qs = as_const(a.q_start)[r], qe = as_const(a.q_start)[r + 1];
   const int G = a.group;
   const int nrows = (qe - qs) * G;
-  const int row0 = qtile * kPrefillRows;
+  const int row0 = qtile * BM;
   if (row0 >= nrows) return;
-  const int qp0 = a.q_pos0[r];
+  const int qp0 = as_const(a.q_pos0)[r];
 
   if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_base, a.inv_freq);
   __syncthreads();
 
   const int h2 = lane >> 5;
-  const int prow = row0 + wave * 32 + (lane & 31);
-  const bool rvalid = prow < nrows;
-  const int tok = rvalid ? prow / G : 0;
-  const int head = g * G + (rvalid ? prow % G : 0);
-  const int qpos = qp0 + tok;
-  const int last = min(row0 + kPrefillRows, nrows) - 1;
+  bool rvalid[RB];
+  int tok[RB], head[RB], qpos[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int prow = row0 + wave * 32 * RB + 32 * rb + (lane & 31);
+    rvalid[rb] = prow < nrows;
+    tok[rb] = rvalid[rb] ? prow / G : 0;
+    head[rb] = g * G + (rvalid[rb] ? prow % G : 0);
+    qpos[rb] = qp0 + tok[rb];
+  }
+  const int last = min(row0 + BM, nrows) - 1;
   const int qmin = qp0 + row0 / G, qmax = qp0 + last / G;
 
-  bf16x8 qf[D / 16];
-  {
-    const uint16_t* qrow = a.q + ((int64_t)(qs + tok) * a.hq + head) * D;
+  bf16x8 qf[RB][D / 16];
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s) qf[s] = q_fragment<D>(qrow, 8 * s + 4 * h2, qpos, sm.freq, rvalid);
+  for (int rb = 0; rb < RB; ++rb) {
+    const uint16_t* qrow = a.q + ((int64_t)(qs + tok[rb]) * a.hq + head[rb]) * D;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) qf[rb][s] = q_fragment<D>(qrow, 8 * s + 4 * h2, qpos[rb], sm.freq, rvalid[rb]);
   }
 
-  f32x16 o[D / 32];
+  f32x16 o[RB][D / 32];
+  float m2[RB], lsum[RB];
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db) o[db] = f32x16{};
-  float m2 = -INFINITY, lsum = 0.f;
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) o[rb][db] = f32x16{};
+    m2[rb] = -INFINITY;
+    lsum[rb] = 0.f;
+  }
   const float c = a.scale_log2;
 
-  Loader<D, 1, ROT> ld;
-  ld.init(tid, sm);
+  PLoader<D, ROT, NT, RB == 2> ld;
+  ld.init(tid, sm.csd, sm.freq);
   TileIter<kSub> it;
-  it.init(a.chunks, a.chunk_start[r], a.chunk_start[r + 1], split, a.splits);
+  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
   bool have = it.seek(a.causal, qmax);
-  if (have) ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
-                     min(kSub, it.cur.len - it.j0));
+
+  // Tile "ahead" state for NBUF == 2: position of the tile after the current one.
+  TileIter<kSub> ahead = it;
+  bool have_ahead = false;
+  if (have) {
+    ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+             min(kSub, it.cur.len - it.j0));
+    if (NBUF == 2) {
+      if (ROT) prefill_base<D>(sm.csb[0], sm.freq, tid, it.cur.pos + it.j0);
+      ahead.step();
+      have_ahead = ahead.seek(a.causal, qmax);
+      if (ROT && have_ahead) prefill_base<D>(sm.csb[1], sm.freq, tid, ahead.cur.pos + ahead.j0);
+      __syncthreads();
+      ld.store(sm.k[0], sm.v[0], sm.csb[0], sm.csd);
+      __syncthreads();
+    }
+  }
+  int parity = 0;
   while (have) {
     const int nvalid = min(kSub, it.cur.len - it.j0);
     const int b0 = it.cur.pos + it.j0;
-    it.step();
-    const bool have_next = it.seek(a.causal, qmax);
-    if (ROT) compute_base<D, 1>(sm, tid, b0);
-    __syncthreads();
-    ld.store(sm);
-    __syncthreads();
-    if (have_next)
-      ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
-               min(kSub, it.cur.len - it.j0));
+    int cur_buf = 0;
+    bool have_next;
+    if (NBUF == 1) {
+      it.step();
+      have_next = it.seek(a.causal, qmax);
+      if (ROT) prefill_base<D>(sm.csb[0], sm.freq, tid, b0);
+      __syncthreads();
+      ld.store(sm.k[0], sm.v[0], sm.csb[0], sm.csd);
+      __syncthreads();
+      if (have_next)
+        ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+                 min(kSub, it.cur.len - it.j0));
+    } else {
+      cur_buf = parity;
+      it = ahead;  // the next tile
+      have_next = have_ahead;
+      if (have_next) {
+        ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+                 min(kSub, it.cur.len - it.j0));
+        ahead.step();
+        have_ahead = ahead.seek(a.causal, qmax);
+      }
+    }
+    const uint16_t* kb = sm.k[cur_buf];
+    // Transposing-read address of this lane in the V tile: row 4*(g/2) + i/4 (+ 16 per key step, + 8 for the
+    // second half of the fragment), column 16*(g%2) + 4*(i%4) (+ 32 per dimension block); g = lane/16, i = lane%16.
+    const uint16_t* vlane = sm.v[cur_buf] + (4 * ((lane >> 4) >> 1) + ((lane & 15) >> 2)) * S::VLD +
+                            16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-    // S^T = K Q^T: two 32-key blocks.
-    f32x16 sa[2] = {f32x16{}, f32x16{}};
+    // S^T = K Q^T: two 32-key blocks per row block; each K fragment feeds RB MFMAs.  Fragments are read one
+    // k-step ahead and the scheduler is fenced per k-step, which bounds the registers held by in-flight reads.
+    f32x16 sa[RB][2];
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s) {
+    for (int rb = 0; rb < RB; ++rb) sa[rb][0] = sa[rb][1] = f32x16{};
+    {
+      const uint16_t* kl = kb + (lane & 31) * S::KLD;
+      u32x4 kv[2][2];
 #pragma unroll
-      for (int blk = 0; blk < 2; ++blk) {
-        const u32x4 kv =
-            *reinterpret_cast<const u32x4*>(sm.k + (32 * blk + (lane & 31)) * S::KLD + 8 * kblk(2 * s + h2));
-        sa[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[s], sa[blk], 0, 0, 0);
+      for (int blk = 0; blk < 2; ++blk)
+        kv[0][blk] = *reinterpret_cast<const u32x4*>(kl + 32 * blk * S::KLD + 8 * kblk_t<NT / kSub>(h2));
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        if (s + 1 < D / 16) {
+#pragma unroll
+          for (int blk = 0; blk < 2; ++blk)
+            kv[(s + 1) & 1][blk] = *reinterpret_cast<const u32x4*>(kl + 32 * blk * S::KLD +
+                                                                   8 * kblk_t<NT / kSub>(2 * (s + 1) + h2));
+        }
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            sa[rb][blk] =
+                __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv[s & 1][blk]), qf[rb][s], sa[rb][blk], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     if (nvalid < kSub || (a.causal && b0 + kSub - 1 > qmin)) {
 #pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int kk = 32 * blk + 8 * (i >> 2) + 4 * h2 + (i & 3);
+            const bool ok = kk < nvalid && (!a.causal || b0 + kk <= qpos[rb]);
+            if (!ok) sa[rb][blk][i] = -INFINITY;
+          }
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sa[rb][blk][i]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      // Lazy rescale: the reference max only moves when this tile's max exceeds it by more than kRescaleSlack.
+      const float mt = mx * c;
+      if (__any(mt > m2[rb] + kRescaleSlack)) {
+        const float mnew = fmaxf(m2[rb], mt);
+        const float alpha = m2[rb] == -INFINITY ? 0.f : fast_exp2(m2[rb] - mnew);
+        lsum[rb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) o[rb][db] *= alpha;
+        m2[rb] = mnew;
+      }
+      const float muse = m2[rb] == -INFINITY ? 0.f : m2[rb];
+      float ps = 0.f;
+#pragma unroll
       for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int kk = 32 * blk + 8 * (i >> 2) + 4 * h2 + (i & 3);
-          const bool ok = kk < nvalid && (!a.causal || b0 + kk <= qpos);
-          if (!ok) sa[blk][i] = -INFINITY;
+          const float p = fast_exp2(fmaf(sa[rb][blk][i], c, -muse));
+          sa[rb][blk][i] = p;
+          ps += p;
         }
+      lsum[rb] += ps;
     }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sa[blk][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    // Lazy rescale: the running reference max m2 only moves when this tile's max exceeds it by more than
-    // kRescaleSlack (log2 units), so probabilities stay below 2^kRescaleSlack and O is rarely touched.
-    const float mt = mx * c;
-    if (__any(mt > m2 + kRescaleSlack)) {
-      const float mnew = fmaxf(m2, mt);
-      const float alpha = m2 == -INFINITY ? 0.f : fast_exp2(m2 - mnew);
-      lsum *= alpha;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) o[db] *= alpha;
-      m2 = mnew;
-    }
-    const float muse = m2 == -INFINITY ? 0.f : m2;
-    float ps = 0.f;
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = fast_exp2(fmaf(sa[blk][i], c, -muse));
-        sa[blk][i] = p;
-        ps += p;
-      }
-    lsum += ps;
 
-    // O^T += V^T P^T: four 16-key steps.
+    // O^T += V^T P^T: four 16-key steps; each V fragment feeds RB MFMAs (same bounded read-ahead).
 #pragma unroll
     for (int s2 = 0; s2 < 4; ++s2) {
-      const f32x16& sv = sa[s2 >> 1];
-      const int b = 8 * (s2 & 1);
-      const bf16x8 pb = as_bf16x8(u32x4{pack2(sv[b + 0], sv[b + 1]), pack2(sv[b + 2], sv[b + 3]),
-                                        pack2(sv[b + 4], sv[b + 5]), pack2(sv[b + 6], sv[b + 7])});
+      bf16x8 pb[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const f32x16& sv = sa[rb][s2 >> 1];
+        const int bq = 8 * (s2 & 1);
+        pb[rb] = as_bf16x8(u32x4{pack2(sv[bq + 0], sv[bq + 1]), pack2(sv[bq + 2], sv[bq + 3]),
+                                 pack2(sv[bq + 4], sv[bq + 5]), pack2(sv[bq + 6], sv[bq + 7])});
+      }
+      u32x4 vv[D / 32];
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        const int vrow = 32 * db + (lane & 31);
-        const u32x4 vv = *reinterpret_cast<const u32x4*>(sm.vt + vrow * S::VLD + vt_off<S::VNB>(vrow, 2 * s2 + h2));
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pb, o[db], 0, 0, 0);
+        const u32x2 lo = tr_read(vlane + (16 * s2) * S::VLD + 32 * db);
+        const u32x2 hi = tr_read(vlane + (16 * s2 + 8) * S::VLD + 32 * db);
+        vv[db] = u32x4{lo[0], lo[1], hi[0], hi[1]};
       }
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          o[rb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv[db]), pb[rb], o[rb][db], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+
+    if (NBUF == 2) {
+      // Base angles two tiles ahead go to the table slot this tile used; the next tile goes to the other buffer.
+      if (ROT && have_ahead) prefill_base<D>(sm.csb[parity], sm.freq, tid, ahead.cur.pos + ahead.j0);
+      if (have_next) ld.store(sm.k[parity ^ 1], sm.v[parity ^ 1], sm.csb[parity ^ 1], sm.csd);
+      __syncthreads();
+      parity ^= 1;
     }
     have = have_next;
   }
 
-  const float ltot = lsum + __shfl_xor(lsum, 32);
-  if (!rvalid) return;
-  const int64_t orow = (int64_t)(qs + tok) * a.hq + head;
-  if (a.splits == 1) {
-    const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
-    uint16_t* dst = a.out + orow * D;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+  for (int rb = 0; rb < RB; ++rb) {
+    const float ltot = lsum[rb] + __shfl_xor(lsum[rb], 32);
+    if (!rvalid[rb]) continue;
+    const int64_t orow = (int64_t)(qs + tok[rb]) * a.hq + head[rb];
+    if (a.splits == 1) {
+      const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
+      uint16_t* dst = a.out + orow * D;
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int dim = 32 * db + 8 * q4 + 4 * h2;
-        *reinterpret_cast<u32x2*>(dst + dim) =
-            u32x2{pack2(o[db][4 * q4] * inv, o[db][4 * q4 + 1] * inv),
-                  pack2(o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv)};
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int dim = 32 * db + 8 * q4 + 4 * h2;
+          *reinterpret_cast<u32x2*>(dst + dim) =
+              u32x2{pack2(o[rb][db][4 * q4] * inv, o[rb][db][4 * q4 + 1] * inv),
+                    pack2(o[rb][db][4 * q4 + 2] * inv, o[rb][db][4 * q4 + 3] * inv)};
+        }
+      if (a.lse && h2 == 0) a.lse[orow] = ltot > 0.f ? (m2[rb] + log2f(ltot)) * kLn2 : -INFINITY;
+    } else {
+      const int64_t wrow = (int64_t)split * a.total_q * a.hq + orow;
+      float* dst = a.ws_acc + wrow * D;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int dim = 32 * db + 8 * q4 + 4 * h2;
+          *reinterpret_cast<f32x4*>(dst + dim) =
+              f32x4{o[rb][db][4 * q4], o[rb][db][4 * q4 + 1], o[rb][db][4 * q4 + 2], o[rb][db][4 * q4 + 3]};
+        }
+      if (h2 == 0) {
+        a.ws_ml[2 * wrow] = m2[rb] * kLn2;
+        a.ws_ml[2 * wrow + 1] = ltot;
       }
-    if (a.lse && h2 == 0) a.lse[orow] = ltot > 0.f ? (m2 + log2f(ltot)) * kLn2 : -INFINITY;
-  } else {
-    const int64_t wrow = (int64_t)split * a.total_q * a.hq + orow;
-    float* dst = a.ws_acc + wrow * D;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int dim = 32 * db + 8 * q4 + 4 * h2;
-        *reinterpret_cast<f32x4*>(dst + dim) =
-            f32x4{o[db][4 * q4], o[db][4 * q4 + 1], o[db][4 * q4 + 2], o[db][4 * q4 + 3]};
-      }
-    if (h2 == 0) {
-      a.ws_ml[2 * wrow] = m2 * kLn2;
-      a.ws_ml[2 * wrow + 1] = ltot;
     }
   }
 }
@@ -535,8 +756,8 @@ __attribute__((amdgpu_waves_per_eu(LAZY_PREFILL_WAVES_PER_EU, LAZY_PREFILL_WAVES
 // Decode: workgroup = (KV split, KV head x head group, request).  Tiles of 128 keys; wave w owns keys
 // 32w..32w+31 of each tile and keeps its own softmax state for up to 16 query heads (one head per MFMA column);
 // the four waves are merged through LDS at the end.  Rows of the 16x16 S^T blocks map to tile keys through
-// kappa(b, r) = 16*(r/8) + r%8 + 8b so that each lane's eight probabilities are, in order, the eight keys the
-// V^T tile holds at its virtual key positions.
+// kappa(b, r) = 16*(r/8) + r%8 + 8b, so each lane's four probabilities of a block are four consecutive keys, which
+// is what one transposing read of V delivers.
 // ---------------------------------------------------------------------------------------------------------------
 __device__ __forceinline__ int kappa(int b, int r) { return 16 * (r >> 3) + (r & 7) + 8 * b; }
 
@@ -551,7 +772,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
   const int G = a.group;
   const int hcount = min(kDecodeHeadsPerGroup, G - kDecodeHeadsPerGroup * hg);
   const int col = lane & 15, kq = lane >> 4;
-  const int qpos = a.q_pos0[r];
+  const int qpos = as_const(a.q_pos0)[r];
 
   if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_base, a.inv_freq);
   __syncthreads();
@@ -574,8 +795,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
 
   Loader<D, 2, ROT> ld;
   ld.init(tid, sm);
+  // Transposing-read address of this lane in the V tile (keys of this wave: kappa order, see above):
+  // row 32*wave + 16*(kq/2) + 4*(kq%2) + i/4 (+ 8 for the second half), column 4*(i%4) (+ 16 per dim block).
+  const uint16_t* vlane =
+      sm.v + (32 * wave + 16 * (kq >> 1) + 4 * (kq & 1) + ((lane & 15) >> 2)) * S::VLD + 4 * (lane & 3);
   TileIter<2 * kSub> it;
-  it.init(a.chunks, a.chunk_start[r], a.chunk_start[r + 1], split, a.splits);
+  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
   bool have = it.seek(a.causal, qpos);
   if (have) ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
                      min(2 * kSub, it.cur.len - it.j0));
@@ -643,8 +868,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
                                       pack2(sa[1][0], sa[1][1]), pack2(sa[1][2], sa[1][3])});
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) {
-      const int vrow = 16 * db + col;
-      const u32x4 vv = *reinterpret_cast<const u32x4*>(sm.vt + vrow * S::VLD + vt_off<S::VNB>(vrow, 4 * wave + kq));
+      const u32x2 lo = tr_read(vlane + 16 * db);
+      const u32x2 hi = tr_read(vlane + 8 * S::VLD + 16 * db);
+      const u32x4 vv = u32x4{lo[0], lo[1], hi[0], hi[1]};
       o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vv), pb, o[db], 0, 0, 0);
     }
     have = have_next;
@@ -780,7 +1006,7 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
   __shared__ double freq[D / 2];
   __shared__ float2 cs[D / 2];
   const int tid = threadIdx.x;
-  const Rec rc = load_rec(in + blockIdx.z);
+  const Rec rc = load_rec(as_const(in) + blockIdx.z);
   const int g = blockIdx.y, j0 = blockIdx.x * kSub;
   if (j0 >= rc.len) return;
   if (tid < D / 2) {
@@ -811,10 +1037,21 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
   }
 }
 
+// 256-row prefill workgroups: eight waves x one 32-row block, or four waves x two blocks.
+#ifndef LAZY_PREFILL_BIG_WAVES
+#define LAZY_PREFILL_BIG_WAVES 8
+#endif
 template <int D, bool ROT>
 hipError_t prefill_d(const AttnArgs& a, hipStream_t st) {
   const dim3 grid(a.q_tiles, a.hkv, a.batch * a.splits);
-  hipLaunchKernelGGL((prefill_kernel<D, ROT>), grid, dim3(kThreads), 0, st, a);
+  if constexpr (D == 128) {
+    if (a.row_blocks == 2) {
+      hipLaunchKernelGGL((prefill_kernel<D, ROT, LAZY_PREFILL_BIG_WAVES, 2, 8 / LAZY_PREFILL_BIG_WAVES>), grid,
+                         dim3(64 * LAZY_PREFILL_BIG_WAVES), 0, st, a);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((prefill_kernel<D, ROT, 4, 1, 1>), grid, dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 
