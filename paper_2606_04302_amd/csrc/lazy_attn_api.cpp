@@ -10,7 +10,6 @@
 namespace {
 
 constexpr int kNumCUs = 256;              // MI355X compute units
-constexpr int kTargetWorkgroups = 1024;  // 256 CUs x ~4 resident workgroups
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -62,9 +61,10 @@ int decode_head_groups(const lazy_attn_params_t* p) {
 
 int decode_splits(const lazy_attn_params_t* p, int32_t batch, int32_t max_kv_len) {
   if (p->num_splits > 0) return p->num_splits;
+  // Two streaming workgroups per CU; split only when the batch alone cannot fill the chip.
   const int64_t base = (int64_t)batch * p->num_kv_heads * decode_head_groups(p);
   const int64_t tiles = ceil_div(max_kv_len, lazy::kDecodeTileKeys);
-  int64_t s = base > 0 ? ceil_div(2 * kTargetWorkgroups, base) : 1;
+  int64_t s = base > 0 ? ceil_div(2 * kNumCUs, base) : 1;
   const int64_t cap = tiles / 2 > 1 ? tiles / 2 : 1;
   if (s > cap) s = cap;
   if (s > 64) s = 64;

@@ -55,7 +55,6 @@ constexpr float kRescaleSlack = 8.0f;
 constexpr double kInvTwoPi = 0.15915494309189533577;
 
 static_assert(kPrefillTileKeys == kSub, "prefill tiles are one loader sub-tile");
-static_assert(kDecodeTileKeys == 2 * kSub, "decode tiles are two loader sub-tiles");
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -173,32 +172,29 @@ struct TileIter {
   }
 };
 
-// LDS of one workgroup.  Bank-conflict notes (64 lanes, 4-byte banks; a 16-byte access pattern is conflict free
-// when every group of 8 consecutive lanes covers distinct 16-byte bank groups):
+// Angles: the rotation of key j of a chunk (position pos + j) uses one decomposition everywhere (lazy kernels and
+// the materialising copy), so every path produces bit-identical rotated keys:
+//     angle(pos + j) = base(pos + 32 * floor(j / 32)) + row(j mod 32)
+// with cos/sin of each part from rope_cs and one angle addition (rotate_pair).
+constexpr int kAngleRows = 32;
+
+// LDS layout constants of a 64-key prefill tile.  Bank-conflict notes (4-byte banks; a 16-byte access pattern is
+// conflict free when every group of 8 consecutive lanes covers distinct 16-byte bank groups):
 //  - K tile rows are D + 8 elements apart (a 4-bank shift per row); the 16-byte blocks of a row are permuted by
-//    kblk() so that the four loader threads writing one row do not collide.
+//    kblk_t() so that the loader threads writing one row do not collide.
 //  - The V tile is row-major (key, dimension) with rows D + 16 elements apart: the 16-byte writes of a row are
 //    contiguous, and the transposing reads (ds_read_b64_tr_b16: 16 lanes read 4 rows x 32 bytes) hit 4 disjoint
 //    8-bank groups.
 //  - cos/sin tables interleave (c, s) and leave 8 floats of gap per loader quarter and a 4-float row tail so that
 //    the 16-byte reads of the threads of one 8-lane group hit distinct banks.
-template <int D, int NSUB>
-struct Smem {
-  static constexpr int KEYS = kSub * NSUB;
-  static constexpr int KLD = D + kPad;       // K tile: [KEYS][KLD], head dimension in virtual order
-  static constexpr int VLD = D + 16;         // V tile: [KEYS][VLD], natural layout
-  static constexpr int PP = D / 8;           // rotation pairs per loader thread
-  static constexpr int CSW = D + 32;         // floats per cos/sin row: (c, s) of pair t at 2t + 8 * (t / PP)
+template <int D>
+struct TileLayout {
+  static constexpr int KLD = D + kPad;       // K tile: [64][KLD], head dimension in virtual order
+  static constexpr int VLD = D + 16;         // V tile: [64][VLD], natural layout
+  static constexpr int CSW = D + 32;         // floats per cos/sin row: (c, s) of pair t at 2t + 8 * (t / (D / 8))
   static constexpr int CSD_LD = CSW + 4;     // row stride of the per-row table (4 banks of shift per row)
-  uint16_t k[KEYS * KLD] __attribute__((aligned(16)));
-  uint16_t v[KEYS * VLD] __attribute__((aligned(16)));
-  float csd[kSub * CSD_LD] __attribute__((aligned(16)));  // cos/sin(delta theta_t) for tile rows delta < 64
-  float csb[NSUB][CSW] __attribute__((aligned(16)));      // cos/sin(b_s theta_t) of the current sub-tile bases
-  double freq[D / 2];                                     // theta_t / 2pi
 };
 
-// Physical position of 16-byte block b of a K tile row.
-__device__ __forceinline__ int kblk(int b) { return b ^ (((b >> 3) & 1) << 1); }
 // Transposing LDS read (gfx950 ds_read_b64_tr_b16).  Within each group of 16 lanes, lane i supplies the address
 // of 4 consecutive 16-bit elements M[i][0..3]; lane j receives M[4e + j/4][j%4] for e = 0..3.  With lane i pointing
 // at row (base + i/4) and column (4 * (i%4)) of a row-major tile, lane j gets column j of rows base..base+3, which is
@@ -210,126 +206,6 @@ __device__ __forceinline__ u32x2 tr_read(const uint16_t* p) {
 }
 template <int D>
 __device__ __forceinline__ int cs_idx(int t) { return 2 * t + 8 * (t / (D / 8)); }
-
-// Cooperative tile loader: 256 threads bring NSUB sub-tiles of 64 keys into LDS, rotating K if ROT.
-// K: thread = (row = tid/4, quarter = tid%4) handles pairs t in [quarter*D/8, (quarter+1)*D/8).
-// V: thread = (dim group = tid % (D/8), key group = tid / (D/8)) handles 4 keys x 8 dims.
-template <int D, int NSUB, bool ROT>
-struct Loader {
-  static constexpr int PP = D / 8;
-  static constexpr int NV = PP / 8;
-  static constexpr int VC = kSub * (D / 8) / kThreads;  // 16-byte V chunks per thread and sub-tile
-  using S = Smem<D, NSUB>;
-  u32x4 klo[NSUB][NV], khi[NSUB][NV];
-  u32x4 vr[NSUB][VC];
-  int tid, row, quarter;
-
-  // Per-row angle table: written once per workgroup (visible after the caller's next barrier).
-  __device__ void init(int t, S& sm) {
-    tid = t;
-    row = t >> 2;
-    quarter = t & 3;
-    if (ROT) {
-      float* cd = sm.csd + row * S::CSD_LD;
-#pragma unroll
-      for (int e = 0; e < PP; ++e) {
-        const int tt = quarter * PP + e;
-        *reinterpret_cast<float2*>(cd + cs_idx<D>(tt)) = rope_cs(row, sm.freq[tt]);
-      }
-    }
-  }
-
-  // Global loads of one tile: kbase / vbase = K / V of this head at the tile's first key (nvalid >= 1 rows).
-  // Rows past the chunk's end read row 0 instead and are zeroed: straight-line code keeps the prefetch buffers in
-  // registers.
-  __device__ void fetch(const uint16_t* kbase, const uint16_t* vbase, int nvalid) {
-    const u32x4 zero = {0, 0, 0, 0};
-    if (nvalid >= NSUB * kSub) {
-#pragma unroll
-      for (int s = 0; s < NSUB; ++s) {
-        const uint16_t* src = kbase + (size_t)(s * kSub + row) * D + quarter * PP;
-#pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          klo[s][v] = reinterpret_cast<const u32x4*>(src)[v];
-          khi[s][v] = reinterpret_cast<const u32x4*>(src + D / 2)[v];
-        }
-#pragma unroll
-        for (int i = 0; i < VC; ++i) {
-          const int c = tid + kThreads * i;
-          vr[s][i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)(s * kSub + c / (D / 8)) * D + 8 * (c % (D / 8)));
-        }
-      }
-      return;
-    }
-#pragma unroll
-    for (int s = 0; s < NSUB; ++s) {
-      const int r = s * kSub + row;
-      const bool ok = r < nvalid;
-      const uint16_t* src = kbase + (size_t)(ok ? r : 0) * D + quarter * PP;
-#pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const u32x4 lo = reinterpret_cast<const u32x4*>(src)[v];
-        const u32x4 hi = reinterpret_cast<const u32x4*>(src + D / 2)[v];
-        klo[s][v] = ok ? lo : zero;
-        khi[s][v] = ok ? hi : zero;
-      }
-#pragma unroll
-      for (int i = 0; i < VC; ++i) {
-        const int c = tid + kThreads * i;
-        const int rr = s * kSub + c / (D / 8);
-        const bool vok = rr < nvalid;
-        const u32x4 x = *reinterpret_cast<const u32x4*>(vbase + (size_t)(vok ? rr : 0) * D + 8 * (c % (D / 8)));
-        vr[s][i] = vok ? x : zero;
-      }
-    }
-  }
-
-  __device__ void store(S& sm) {
-#pragma unroll
-    for (int s = 0; s < NSUB; ++s) {
-      uint16_t* krow = sm.k + (s * kSub + row) * S::KLD;
-      const float* cb = sm.csb[s];
-      const float* cd = sm.csd + row * S::CSD_LD;
-#pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int t0 = quarter * PP + 8 * v;  // first pair of this 8-pair group
-        u32x4 w0, w1;
-        if (ROT) {
-          float yl[8], yh[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const uint32_t wl = klo[s][v][e >> 1], wh = khi[s][v][e >> 1];
-            const float x1 = (e & 1) ? bf_hi(wl) : bf_lo(wl);
-            const float x2 = (e & 1) ? bf_hi(wh) : bf_lo(wh);
-            const int ci = cs_idx<D>(t0 + e);
-            rotate_pair(x1, x2, *reinterpret_cast<const float2*>(cb + ci), *reinterpret_cast<const float2*>(cd + ci),
-                        yl[e], yh[e]);
-          }
-          w0 = u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yh[0], yh[1]), pack2(yh[2], yh[3])};
-          w1 = u32x4{pack2(yl[4], yl[5]), pack2(yl[6], yl[7]), pack2(yh[4], yh[5]), pack2(yh[6], yh[7])};
-        } else {
-          w0 = u32x4{klo[s][v][0], klo[s][v][1], khi[s][v][0], khi[s][v][1]};
-          w1 = u32x4{klo[s][v][2], klo[s][v][3], khi[s][v][2], khi[s][v][3]};
-        }
-        *reinterpret_cast<u32x4*>(krow + 8 * kblk(t0 / 4)) = w0;
-        *reinterpret_cast<u32x4*>(krow + 8 * kblk(t0 / 4 + 1)) = w1;
-      }
-#pragma unroll
-      for (int i = 0; i < VC; ++i) {
-        const int c = tid + kThreads * i;
-        *reinterpret_cast<u32x4*>(sm.v + (s * kSub + c / (D / 8)) * S::VLD + 8 * (c % (D / 8))) = vr[s][i];
-      }
-    }
-  }
-};
-
-template <int D, int NSUB>
-__device__ __forceinline__ void compute_base(Smem<D, NSUB>& sm, int tid, int b0) {
-  for (int e = tid; e < NSUB * (D / 2); e += kThreads) {
-    const int s = e / (D / 2), t = e % (D / 2);
-    *reinterpret_cast<float2*>(sm.csb[s] + cs_idx<D>(t)) = rope_cs(b0 + s * kSub, sm.freq[t]);
-  }
-}
 
 // Load 4 query pairs (t0..t0+3 with their partners t0+D/2..) of one query row, rotated at position p, as one
 // 8-element MFMA fragment in virtual order [low t0..t0+3, high t0..t0+3].
@@ -372,11 +248,11 @@ __device__ __forceinline__ int xcd_remap(int id, int n) {
 
 template <int D, int NBUF>
 struct PrefillSmem {
-  using S = Smem<D, 1>;
+  using S = TileLayout<D>;
   uint16_t k[NBUF][kSub * S::KLD] __attribute__((aligned(16)));
   uint16_t v[NBUF][kSub * S::VLD] __attribute__((aligned(16)));
-  float csd[kSub * S::CSD_LD] __attribute__((aligned(16)));
-  float csb[2][S::CSW] __attribute__((aligned(16)));
+  float csd[kAngleRows * S::CSD_LD] __attribute__((aligned(16)));  // cos/sin(delta theta_t), delta < 32
+  float csb[2][2][S::CSW] __attribute__((aligned(16)));            // [tile parity][half]: cos/sin(base theta_t)
   double freq[D / 2];
 };
 
@@ -392,7 +268,7 @@ __device__ __forceinline__ int kblk_t(int b) {
 // The per-row cos/sin constants are written to a private LDS slice once per workgroup and read per tile.
 template <int D, bool ROT, int NT, bool CSD_REGS = false>
 struct PLoader {
-  using S = Smem<D, 1>;
+  using S = TileLayout<D>;
   static constexpr int TPR = NT / kSub;
   static constexpr int PP = D / (2 * TPR);
   static constexpr int NV = PP / 8;
@@ -403,22 +279,27 @@ struct PLoader {
   float2 cdr[CSD_REGS && ROT ? PP : 1];
   int tid, row, part;
 
+  // Writes the per-row angle table (rows < 32); it is read after the caller's next barrier.
   __device__ void init(int t, float* csd, const double* freq) {
     tid = t;
     row = t / TPR;
     part = t % TPR;
-    if (ROT) {
+    if (ROT && row < kAngleRows) {
       float* cd = csd + row * S::CSD_LD;
 #pragma unroll
       for (int e = 0; e < PP; ++e) {
         const int tt = part * PP + e;
         *reinterpret_cast<float2*>(cd + cs_idx<D>(tt)) = rope_cs(row, freq[tt]);
       }
-      // Read back once: the loop writes LDS, so these registers cannot be re-derived inside it.
-      if (CSD_REGS) {
+    }
+  }
+  // With CSD_REGS, after that barrier: keep this thread's per-row constants in registers (the loop writes LDS, so
+  // they cannot be re-derived inside it).
+  __device__ void load_constants(const float* csd) {
+    if (ROT && CSD_REGS) {
+      const float* cd = csd + (row & (kAngleRows - 1)) * S::CSD_LD;
 #pragma unroll
-        for (int e = 0; e < PP; ++e) cdr[e] = *reinterpret_cast<const float2*>(cd + cs_idx<D>(part * PP + e));
-      }
+      for (int e = 0; e < PP; ++e) cdr[e] = *reinterpret_cast<const float2*>(cd + cs_idx<D>(part * PP + e));
     }
   }
 
@@ -457,9 +338,11 @@ struct PLoader {
     }
   }
 
-  __device__ void store(uint16_t* kbuf, uint16_t* vtbuf, const float* cb, const float* csd) {
+  // cb: the tile's two base tables [2][CSW] (rows 0..31 and 32..63).
+  __device__ void store(uint16_t* kbuf, uint16_t* vtbuf, const float* cb2, const float* csd) {
     uint16_t* krow = kbuf + row * S::KLD;
-    const float* cd = csd + row * S::CSD_LD;
+    const float* cb = cb2 + (row / kAngleRows) * S::CSW;
+    const float* cd = csd + (row & (kAngleRows - 1)) * S::CSD_LD;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int t0 = part * PP + 8 * v;
@@ -491,16 +374,20 @@ struct PLoader {
   }
 };
 
+// Base tables of a 64-key tile whose first key sits at position b0: [0] for rows 0..31, [1] for rows 32..63.
 template <int D>
-__device__ __forceinline__ void prefill_base(float* csb, const double* freq, int tid, int b0) {
-  if (tid < D / 2) *reinterpret_cast<float2*>(csb + cs_idx<D>(tid)) = rope_cs(b0, freq[tid]);
+__device__ __forceinline__ void prefill_base(float* csb2, const double* freq, int tid, int b0) {
+  if (tid < D) {
+    const int h = tid / (D / 2), t = tid % (D / 2);
+    *reinterpret_cast<float2*>(csb2 + h * TileLayout<D>::CSW + cs_idx<D>(t)) = rope_cs(b0 + kAngleRows * h, freq[t]);
+  }
 }
 
 template <int D, bool ROT, int NW, int NBUF, int RB>
 __global__ __launch_bounds__(NW * 64)
 __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void prefill_kernel(AttnArgs a) {
   __shared__ PrefillSmem<D, NBUF> sm;
-  using S = Smem<D, 1>;
+  using S = TileLayout<D>;
   constexpr int NT = NW * 64;
   constexpr int BM = 32 * NW * RB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -555,6 +442,10 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
 
   PLoader<D, ROT, NT, RB == 2> ld;
   ld.init(tid, sm.csd, sm.freq);
+  if constexpr (RB == 2) {
+    __syncthreads();
+    ld.load_constants(sm.csd);
+  }
   TileIter<kSub> it;
   it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
   bool have = it.seek(a.causal, qmax);
@@ -566,12 +457,12 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
              min(kSub, it.cur.len - it.j0));
     if (NBUF == 2) {
-      if (ROT) prefill_base<D>(sm.csb[0], sm.freq, tid, it.cur.pos + it.j0);
+      if (ROT) prefill_base<D>(sm.csb[0][0], sm.freq, tid, it.cur.pos + it.j0);
       ahead.step();
       have_ahead = ahead.seek(a.causal, qmax);
-      if (ROT && have_ahead) prefill_base<D>(sm.csb[1], sm.freq, tid, ahead.cur.pos + ahead.j0);
+      if (ROT && have_ahead) prefill_base<D>(sm.csb[1][0], sm.freq, tid, ahead.cur.pos + ahead.j0);
       __syncthreads();
-      ld.store(sm.k[0], sm.v[0], sm.csb[0], sm.csd);
+      ld.store(sm.k[0], sm.v[0], sm.csb[0][0], sm.csd);
       __syncthreads();
     }
   }
@@ -584,9 +475,9 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     if (NBUF == 1) {
       it.step();
       have_next = it.seek(a.causal, qmax);
-      if (ROT) prefill_base<D>(sm.csb[0], sm.freq, tid, b0);
+      if (ROT) prefill_base<D>(sm.csb[0][0], sm.freq, tid, b0);
       __syncthreads();
-      ld.store(sm.k[0], sm.v[0], sm.csb[0], sm.csd);
+      ld.store(sm.k[0], sm.v[0], sm.csb[0][0], sm.csd);
       __syncthreads();
       if (have_next)
         ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
@@ -707,8 +598,8 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
 
     if (NBUF == 2) {
       // Base angles two tiles ahead go to the table slot this tile used; the next tile goes to the other buffer.
-      if (ROT && have_ahead) prefill_base<D>(sm.csb[parity], sm.freq, tid, ahead.cur.pos + ahead.j0);
-      if (have_next) ld.store(sm.k[parity ^ 1], sm.v[parity ^ 1], sm.csb[parity ^ 1], sm.csd);
+      if (ROT && have_ahead) prefill_base<D>(sm.csb[parity][0], sm.freq, tid, ahead.cur.pos + ahead.j0);
+      if (have_next) ld.store(sm.k[parity ^ 1], sm.v[parity ^ 1], sm.csb[parity ^ 1][0], sm.csd);
       __syncthreads();
       parity ^= 1;
     }
@@ -753,18 +644,95 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
 }
 
 // ---------------------------------------------------------------------------------------------------------------
-// Decode: workgroup = (KV split, KV head x head group, request).  Tiles of 128 keys; wave w owns keys
-// 32w..32w+31 of each tile and keeps its own softmax state for up to 16 query heads (one head per MFMA column);
-// the four waves are merged through LDS at the end.  Rows of the 16x16 S^T blocks map to tile keys through
-// kappa(b, r) = 16*(r/8) + r%8 + 8b, so each lane's four probabilities of a block are four consecutive keys, which
-// is what one transposing read of V delivers.
+// Decode: workgroup = (KV split, KV head x head group, request), four waves that stream independently.  The split's
+// keys are cut into 32-key tiles (never straddling chunks); wave w takes tiles w, w+4, w+8, ... and keeps its own
+// softmax state for up to 16 query heads (one head per MFMA column), with the next tile's K / V already in flight
+// in registers while the current one is processed.  No barrier is needed until the four states are merged.
+//  - K goes straight from global memory into the A-operand layout of v_mfma_f32_16x16x32_bf16 and is rotated in
+//    registers.  Decode uses its own head-dimension order: k-step 2s+h holds, in lane (row, kq), the 8 dims
+//    h*D/2 + 32s + 8kq .. +7, so the two halves of every rotation pair sit in the same lane (two k-steps apart)
+//    and each half is one 16-byte load.
+//  - Block b (0/1) row r of S^T is tile key kappa(b, r) = 16*(r/8) + r%8 + 8b, so a lane's four probabilities of a
+//    block are four consecutive keys: exactly what one transposing read of the row-major V slice delivers.
+//  - Angles: cos/sin((b0 + kappa) theta_t) = base (per tile, one table per wave, computed one tile ahead) x
+//    per-row constants (a 32-row table shared by the workgroup).
 // ---------------------------------------------------------------------------------------------------------------
 __device__ __forceinline__ int kappa(int b, int r) { return 16 * (r >> 3) + (r & 7) + 8 * b; }
 
+constexpr int kDecWaveKeys = 32;
+
+template <int D>
+struct DecodeSmem {
+  static constexpr int VLD = D + 16;                 // V slice row stride (elements)
+  static constexpr int CSD_LD = D + 4;               // per-row cos/sin row stride (floats): 4 banks per row
+  static constexpr int CSB = D + D / 4;              // per-tile base table: (c, s) of pair t at 2t + 4*(t/8)
+  uint16_t v[4][kDecWaveKeys * VLD] __attribute__((aligned(16)));
+  float csd[kDecWaveKeys * CSD_LD] __attribute__((aligned(16)));
+  float csb[4][2][CSB] __attribute__((aligned(16)));
+  double freq[D / 2];
+};
+template <int D>
+__device__ __forceinline__ int csb_idx(int t) { return 2 * t + 4 * (t >> 3); }
+
+// Raw K / V of one wave tile in registers.
+template <int D>
+struct DecTile {
+  static constexpr int SP = D / 64;          // 16-byte groups per half row per lane
+  static constexpr int VC = kDecWaveKeys * (D / 8) / 64;
+  u32x4 k[2][SP][2];                         // [block][s][half]
+  u32x4 v[VC];
+};
+
+template <int D>
+__device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, const uint16_t* vbase, int nvalid,
+                                          int lane) {
+  const int r = lane & 15, kq = lane >> 4;
+  const u32x4 zero = {0, 0, 0, 0};
+  if (nvalid >= kDecWaveKeys) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const uint16_t* row = kbase + (size_t)kappa(b, r) * D + 8 * kq;
+#pragma unroll
+      for (int s = 0; s < DecTile<D>::SP; ++s) {
+        t.k[b][s][0] = *reinterpret_cast<const u32x4*>(row + 32 * s);
+        t.k[b][s][1] = *reinterpret_cast<const u32x4*>(row + D / 2 + 32 * s);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < DecTile<D>::VC; ++i) {
+      const int c = lane + 64 * i;
+      t.v[i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)(c / (D / 8)) * D + 8 * (c % (D / 8)));
+    }
+    return;
+  }
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int key = kappa(b, r);
+    const bool ok = key < nvalid;
+    const uint16_t* row = kbase + (size_t)(ok ? key : 0) * D + 8 * kq;
+#pragma unroll
+    for (int s = 0; s < DecTile<D>::SP; ++s) {
+      const u32x4 lo = *reinterpret_cast<const u32x4*>(row + 32 * s);
+      const u32x4 hi = *reinterpret_cast<const u32x4*>(row + D / 2 + 32 * s);
+      t.k[b][s][0] = ok ? lo : zero;
+      t.k[b][s][1] = ok ? hi : zero;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < DecTile<D>::VC; ++i) {
+    const int c = lane + 64 * i;
+    const int key = c / (D / 8);
+    const bool ok = key < nvalid;
+    const u32x4 x = *reinterpret_cast<const u32x4*>(vbase + (size_t)(ok ? key : 0) * D + 8 * (c % (D / 8)));
+    t.v[i] = ok ? x : zero;
+  }
+}
+
 template <int D, bool ROT>
-__global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
-  __shared__ Smem<D, 2> sm;
-  using S = Smem<D, 2>;
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_kernel(AttnArgs a) {
+  __shared__ DecodeSmem<D> sm;
+  using S = DecodeSmem<D>;
+  constexpr int SP = DecTile<D>::SP;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int split = blockIdx.x;
   const int g = blockIdx.y / a.head_groups, hg = blockIdx.y % a.head_groups;
@@ -776,16 +744,41 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
 
   if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_base, a.inv_freq);
   __syncthreads();
+  if (ROT) {
+    // Per-row constants cos/sin(delta theta_t), delta < 32: 16 per thread.
+    for (int e = tid; e < kDecWaveKeys * (D / 2); e += kThreads) {
+      const int dr = e / (D / 2), t = e % (D / 2);
+      *reinterpret_cast<float2*>(sm.csd + dr * S::CSD_LD + 2 * t) = rope_cs(dr, sm.freq[t]);
+    }
+  }
 
   const bool hvalid = col < hcount;
   const int head = g * G + kDecodeHeadsPerGroup * hg + (hvalid ? col : 0);
+  // Q fragments in the decode head-dimension order, rotated at the query position.
   bf16x8 qf[D / 32];
   {
     const uint16_t* qrow = a.q + ((int64_t)r * a.hq + head) * D;
 #pragma unroll
-    for (int s = 0; s < D / 32; ++s)
-      qf[s] = q_fragment<D>(qrow, 8 * (2 * s + (kq >> 1)) + 4 * (kq & 1), qpos, sm.freq, hvalid);
+    for (int s = 0; s < SP; ++s) {
+      float y1[8], y2[8];
+      const int t0 = 32 * s + 8 * kq;
+      u32x4 lo = {0, 0, 0, 0}, hi = {0, 0, 0, 0};
+      if (hvalid) {
+        lo = *reinterpret_cast<const u32x4*>(qrow + t0);
+        hi = *reinterpret_cast<const u32x4*>(qrow + D / 2 + t0);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x1 = (e & 1) ? bf_hi(lo[e >> 1]) : bf_lo(lo[e >> 1]);
+        const float x2 = (e & 1) ? bf_hi(hi[e >> 1]) : bf_lo(hi[e >> 1]);
+        rotate_q_pair(x1, x2, qpos, sm.freq[t0 + e], y1[e], y2[e]);
+      }
+      qf[2 * s] = as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])});
+      qf[2 * s + 1] =
+          as_bf16x8(u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])});
+    }
   }
+  __syncthreads();  // per-row table complete
 
   f32x4 o[D / 16];
 #pragma unroll
@@ -793,46 +786,82 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
   float m2 = -INFINITY, lsum = 0.f;
   const float c = a.scale_log2;
 
-  Loader<D, 2, ROT> ld;
-  ld.init(tid, sm);
-  // Transposing-read address of this lane in the V tile (keys of this wave: kappa order, see above):
-  // row 32*wave + 16*(kq/2) + 4*(kq%2) + i/4 (+ 8 for the second half), column 4*(i%4) (+ 16 per dim block).
-  const uint16_t* vlane =
-      sm.v + (32 * wave + 16 * (kq >> 1) + 4 * (kq & 1) + ((lane & 15) >> 2)) * S::VLD + 4 * (lane & 3);
-  TileIter<2 * kSub> it;
-  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
-  bool have = it.seek(a.causal, qpos);
-  if (have) ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
-                     min(2 * kSub, it.cur.len - it.j0));
-  while (have) {
-    const int nvalid = min(2 * kSub, it.cur.len - it.j0);
-    const int b0 = it.cur.pos + it.j0;
-    it.step();
-    const bool have_next = it.seek(a.causal, qpos);
-    if (ROT) compute_base<D, 2>(sm, tid, b0);
-    __syncthreads();
-    ld.store(sm);
-    __syncthreads();
-    if (have_next)
-      ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
-               min(2 * kSub, it.cur.len - it.j0));
+  uint16_t* vw = sm.v[wave];
+  // Transposing-read address of this lane in its V slice: row 16*(kq/2) + 4*(kq%2) + i/4 (+ 8 for the second
+  // half), column 4*(i%4) (+ 16 per dimension block); i = lane % 16.
+  const uint16_t* vlane = vw + (16 * (kq >> 1) + 4 * (kq & 1) + ((lane & 15) >> 2)) * S::VLD + 4 * (lane & 3);
+  const float* cd0 = sm.csd + kappa(0, col) * S::CSD_LD;
+  const float* cd1 = sm.csd + kappa(1, col) * S::CSD_LD;
 
-    f32x4 sa[2] = {f32x4{}, f32x4{}};
+  // This wave's tiles: every fourth tile of the split, starting at tile `wave`.
+  TileIter<kDecWaveKeys> it;
+  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
+  for (int k = 0; k < wave && it.left > 0; ++k) it.step();
+  bool have = it.seek(a.causal, qpos);
+  DecTile<D> cur, nxt;
+  int buf = 0;
+  if (have) {
+    dec_fetch<D>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+                 min(kDecWaveKeys, it.cur.len - it.j0), lane);
+    if (ROT && lane < D / 2)
+      *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
+  }
+  while (have) {
+    const int nvalid = min(kDecWaveKeys, it.cur.len - it.j0);
+    const int b0 = it.cur.pos + it.j0;
+    for (int k = 0; k < 4 && it.left > 0; ++k) it.step();
+    const bool have_next = it.seek(a.causal, qpos);
+    if (have_next) {
+      dec_fetch<D>(nxt, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+                   min(kDecWaveKeys, it.cur.len - it.j0), lane);
+      if (ROT && lane < D / 2)
+        *reinterpret_cast<float2*>(sm.csb[wave][buf ^ 1] + csb_idx<D>(lane)) =
+            rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
+    }
+
+    // V of this tile into the wave's LDS slice (row-major).
 #pragma unroll
-    for (int s = 0; s < D / 32; ++s) {
+    for (int i = 0; i < DecTile<D>::VC; ++i) {
+      const int cc = lane + 64 * i;
+      *reinterpret_cast<u32x4*>(vw + (cc / (D / 8)) * S::VLD + 8 * (cc % (D / 8))) = cur.v[i];
+    }
+
+    // Rotate K in registers and form S^T = K Q^T, one pair of k-steps (low / high halves) at a time.
+    f32x4 sa[2] = {f32x4{}, f32x4{}};
+    const float* cb = sm.csb[wave][buf];
+#pragma unroll
+    for (int s = 0; s < SP; ++s) {
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
-        const int key = 32 * wave + kappa(b, col);
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(sm.k + key * S::KLD + 8 * kblk(4 * s + kq));
-        sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kv), qf[s], sa[b], 0, 0, 0);
+        const u32x4 wl = cur.k[b][s][0], wh = cur.k[b][s][1];
+        u32x4 klo, khi;
+        if (ROT) {
+          const float* cdb = b ? cd1 : cd0;
+          float y1[8], y2[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int t = 32 * s + 8 * kq + e;
+            const float x1 = (e & 1) ? bf_hi(wl[e >> 1]) : bf_lo(wl[e >> 1]);
+            const float x2 = (e & 1) ? bf_hi(wh[e >> 1]) : bf_lo(wh[e >> 1]);
+            rotate_pair(x1, x2, *reinterpret_cast<const float2*>(cb + csb_idx<D>(t)),
+                        *reinterpret_cast<const float2*>(cdb + 2 * t), y1[e], y2[e]);
+          }
+          klo = u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])};
+          khi = u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])};
+        } else {
+          klo = wl;
+          khi = wh;
+        }
+        sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(klo), qf[2 * s], sa[b], 0, 0, 0);
+        sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(khi), qf[2 * s + 1], sa[b], 0, 0, 0);
       }
     }
-    if (nvalid < 2 * kSub || (a.causal && b0 + 2 * kSub - 1 > qpos)) {
+    if (nvalid < kDecWaveKeys || (a.causal && b0 + kDecWaveKeys - 1 > qpos)) {
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int kk = 32 * wave + kappa(b, 4 * kq + i);
+          const int kk = kappa(b, 4 * kq + i);
           const bool ok = kk < nvalid && (!a.causal || b0 + kk <= qpos);
           if (!ok) sa[b][i] = -INFINITY;
         }
@@ -866,23 +895,26 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
     lsum += ps;
     const bf16x8 pb = as_bf16x8(u32x4{pack2(sa[0][0], sa[0][1]), pack2(sa[0][2], sa[0][3]),
                                       pack2(sa[1][0], sa[1][1]), pack2(sa[1][2], sa[1][3])});
+    // O^T += V^T P^T from the wave's V slice (same-wave LDS ordering: written above, read here).
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) {
       const u32x2 lo = tr_read(vlane + 16 * db);
       const u32x2 hi = tr_read(vlane + 8 * S::VLD + 16 * db);
-      const u32x4 vv = u32x4{lo[0], lo[1], hi[0], hi[1]};
-      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vv), pb, o[db], 0, 0, 0);
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pb, o[db], 0,
+                                                      0, 0);
     }
+    cur = nxt;
+    buf ^= 1;
     have = have_next;
   }
 
-  // Merge the four waves' states through LDS (the K tile area is free now).
+  // Merge the four waves' states through LDS (the V slices are free once every wave is here).
   float ltot = lsum + __shfl_xor(lsum, 16);
   ltot += __shfl_xor(ltot, 32);
   __syncthreads();
-  float* macc = reinterpret_cast<float*>(sm.k);  // [4][D][16]
-  float* mm = macc + 4 * D * 16;                 // [4][16]
-  float* ml = mm + 4 * 16;                       // [4][16]
+  float* macc = reinterpret_cast<float*>(sm.v[0]);  // [4][D][16]
+  float* mm = macc + 4 * D * 16;                    // [4][16]
+  float* ml = mm + 4 * 16;                          // [4][16]
 #pragma unroll
   for (int db = 0; db < D / 16; ++db)
 #pragma unroll
@@ -1004,15 +1036,14 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
                                                                       uint16_t* __restrict__ k_out) {
   constexpr int PP = D / 8, NV = PP / 8;
   __shared__ double freq[D / 2];
-  __shared__ float2 cs[D / 2];
+  __shared__ float2 cs[2][D / 2];  // base angles of rows 0..31 and 32..63 of this 64-key block
   const int tid = threadIdx.x;
   const Rec rc = load_rec(as_const(in) + blockIdx.z);
   const int g = blockIdx.y, j0 = blockIdx.x * kSub;
   if (j0 >= rc.len) return;
-  if (tid < D / 2) {
-    freq[tid] = theta_rev(tid, D, base, inv_freq);
-    cs[tid] = rope_cs(rc.pos + j0, freq[tid]);
-  }
+  if (tid < D / 2) freq[tid] = theta_rev(tid, D, base, inv_freq);
+  __syncthreads();
+  if (tid < D) cs[tid / (D / 2)][tid % (D / 2)] = rope_cs(rc.pos + j0 + kAngleRows * (tid / (D / 2)), freq[tid % (D / 2)]);
   __syncthreads();
   const int row = tid >> 2, quarter = tid & 3;
   if (j0 + row >= rc.len) return;
@@ -1028,7 +1059,7 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
     for (int e = 0; e < 8; ++e) {
       const float x1 = (e & 1) ? bf_hi(wl[e >> 1]) : bf_lo(wl[e >> 1]);
       const float x2 = (e & 1) ? bf_hi(wh[e >> 1]) : bf_lo(wh[e >> 1]);
-      rotate_pair(x1, x2, cs[t0 + e], rope_cs(row, freq[t0 + e]), yl[e], yh[e]);
+      rotate_pair(x1, x2, cs[row / kAngleRows][t0 + e], rope_cs(row % kAngleRows, freq[t0 + e]), yl[e], yh[e]);
     }
     *reinterpret_cast<u32x4*>(dst + t0) =
         u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yl[4], yl[5]), pack2(yl[6], yl[7])};
