@@ -272,6 +272,7 @@ def main() -> int:
             "plain_decode_ms": round(dplain, 5),
             "materialize_then_attend_ms": round(dmat + dplain, 5),
             "speedup_vs_materialize": round((dmat + dplain) / dms, 3),
+            "traffic": recorded_traffic("decode_kernel_rag_decode"),
         }
         del kmd, dd
 
