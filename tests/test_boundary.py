@@ -1,0 +1,237 @@
+"""CPU tests of the C ABI boundary: exported symbols, struct layouts, host-side table validation, scalar argument
+checks and workspace sizing.  Nothing here launches a kernel."""
+import ctypes
+import os
+import re
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2606_04302_amd import build as B
+from paper_2606_04302_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lazy_attn.h")
+
+
+@pytest.fixture(scope="module")
+def ops():
+    from paper_2606_04302_amd import ops as O
+
+    if not os.path.exists(O.LIB_PATH):
+        B.build()
+    O.lib()
+    return O
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return re.findall(r"LAZY_API\s+[\w\s\*]+?\b(lazy_\w+)\s*\(", text)
+
+
+def test_library_exports_every_declared_symbol(ops):
+    names = declared_functions()
+    assert len(names) >= 11, names
+    lib = ctypes.CDLL(ops.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", ops.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (\w+)", out))
+    assert set(names) <= exported
+    # only the C ABI is exported
+    assert {n for n in exported if not n.startswith("_")} == set(names)
+    assert set(names) == set(ops.SIGNATURES)
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="gcc missing")
+def test_struct_layout_matches_header(tmp_path, ops):
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include <stdio.h>\n#include <stddef.h>\n#include "lazy_attn.h"\n'
+        "int main(void){"
+        'printf("%zu %zu %zu %zu %zu %zu %zu\\n", sizeof(lazy_chunk_t), offsetof(lazy_chunk_t, v_offset),'
+        " offsetof(lazy_chunk_t, len), offsetof(lazy_chunk_t, pos_offset), offsetof(lazy_chunk_t, k_stride),"
+        " offsetof(lazy_chunk_t, v_stride), sizeof(lazy_attn_params_t));"
+        'printf("%zu %zu %zu %zu\\n", offsetof(lazy_attn_params_t, rope_base), offsetof(lazy_attn_params_t, inv_freq),'
+        " offsetof(lazy_attn_params_t, num_splits), offsetof(lazy_attn_params_t, reserved));"
+        "return 0;}"
+    )
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    a, b = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")[:2]
+    c = [int(x) for x in a.split()]
+    p = [int(x) for x in b.split()]
+    LC, LP = ops.LazyChunk, ops.LazyAttnParams
+    assert c == [ctypes.sizeof(LC), LC.v_offset.offset, LC.len.offset, LC.pos_offset.offset, LC.k_stride.offset,
+                 LC.v_stride.offset, ctypes.sizeof(LP)]
+    assert p == [LP.rope_base.offset, LP.inv_freq.offset, LP.num_splits.offset, LP.reserved.offset]
+    dt = W.CHUNK_DTYPE
+    assert [dt.fields[n][1] for n in ("k_offset", "v_offset", "len", "pos_offset", "k_stride", "v_stride")] == [
+        0, c[1], c[2], c[3], c[4], c[5]]
+
+
+def _valid(w, ops, **kw):
+    cfg = ops.config_of(w, **kw)
+    return ops.validate(cfg, w.q_start if w.kind == "prefill" else None, w.q_pos0, w.chunks, w.chunk_start,
+                        w.pool.size, w.pool.size)
+
+
+def test_validate_accepts_generated_workloads(ops):
+    for w in (W.tiny_rag_prefill(), W.rag_prefill(batch=2, n_chunks=3, chunk_len=64, pool_chunks=4, q_len=8, hq=8,
+                                                     hkv=2),
+              W.rag_decode(batch=3, n_chunks=2, chunk_len=70, pool_chunks=3, hq=8, hkv=2),
+              W.varlen_rag(batch=3, pool_chunks=6, len_hi=300, k_lo=2, k_hi=4, q_hi=40, hq=8, hkv=2)):
+        code, bad, why = _valid(w, ops)
+        assert code == ops.LAZY_OK, (w.name, bad, why)
+
+
+def _w():
+    return W.rag_prefill(seed=3, batch=2, hq=4, hkv=2, d=64, prefix_len=8, n_chunks=2, chunk_len=16, pool_chunks=3,
+                         q_len=4)
+
+
+@pytest.mark.parametrize("mutate,reason", [
+    (lambda w: w.chunk_start.__setitem__(0, 1), "chunk_start[0]"),
+    (lambda w: w.chunk_start.__setitem__(1, w.chunk_start[2] + 1), "non-decreasing"),
+    (lambda w: w.chunks["len"].__setitem__(1, 0), "len"),
+    (lambda w: w.chunks["pos_offset"].__setitem__(0, -1), "pos_offset"),
+    (lambda w: w.chunks["pos_offset"].__setitem__(0, (1 << 24) - 3), "LAZY_MAX_POS"),
+    (lambda w: w.chunks["k_stride"].__setitem__(2, 1), "stride"),
+    (lambda w: w.chunks["k_offset"].__setitem__(1, w.chunks["k_offset"][1] + 4), "multiples of 8"),
+    (lambda w: w.chunks["k_offset"].__setitem__(1, w.pool.size - 8), "K range"),
+    (lambda w: w.chunks["v_offset"].__setitem__(1, w.pool.size - 8), "V range"),
+    (lambda w: w.q_start.__setitem__(0, 1), "q_start[0]"),
+    (lambda w: w.q_pos0.__setitem__(1, -5), "query position"),
+    (lambda w: w.chunks["pos_offset"].__setitem__(slice(0, 4), 10 ** 6), "sees no key"),
+])
+def test_validate_rejects_every_contract_violation(ops, mutate, reason):
+    w = _w()
+    assert _valid(w, ops)[0] == ops.LAZY_OK
+    mutate(w)
+    code, bad, why = _valid(w, ops)
+    assert code == ops.LAZY_EDATA and reason in why, (code, bad, why)
+    assert bad >= 0
+
+
+def test_validate_non_causal_request_without_keys(ops):
+    reqs = [dict(chunks=[(4, 0)], q_len=2, q_pos0=4), dict(chunks=[], q_len=3, q_pos0=0)]
+    w = W.custom(1, 2, 1, 64, 1e4, reqs, causal=False)
+    code, bad, why = _valid(w, ops)
+    assert code == ops.LAZY_EDATA and bad == 1 and "no keys" in why
+
+
+def test_scalar_argument_errors_return_before_any_launch(ops):
+    L = ops.lib()
+    P = ops.LazyAttnParams
+    fake = ctypes.c_void_p(0x1000)
+
+    def prefill(p, batch=1, total_q=4, max_q=4, max_kv=16, ws=None, ws_bytes=0, q=fake, out=fake):
+        return L.lazy_attn_prefill(ctypes.byref(p) if p is not None else None, q, fake, fake, fake, fake, fake,
+                                   fake, batch, total_q, max_q, max_kv, out, None, ws, ws_bytes, None)
+
+    good = P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0)
+    assert prefill(None) == ops.LAZY_EINVAL
+    assert prefill(P(8, 3, 128, 1, 1e4, 0.0, None, 0, 0)) == ops.LAZY_EINVAL          # Hq % Hkv != 0
+    assert prefill(P(8, 2, 96, 1, 1e4, 0.0, None, 0, 0)) == ops.LAZY_EUNSUPPORTED     # head_dim
+    assert prefill(P(8, 2, 128, 2, 1e4, 0.0, None, 0, 0)) == ops.LAZY_EINVAL          # causal flag
+    assert prefill(P(8, 2, 128, 1, -1.0, 0.0, None, 0, 0)) == ops.LAZY_EINVAL         # rope base
+    assert prefill(P(8, 2, 128, 1, 1e4, -0.5, None, 0, 0)) == ops.LAZY_EINVAL         # softmax scale
+    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, -1, 0)) == ops.LAZY_EINVAL         # splits
+    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 7)) == ops.LAZY_EINVAL          # reserved
+    assert prefill(good, batch=-1) == ops.LAZY_EINVAL
+    assert prefill(good, batch=0) == ops.LAZY_OK                                       # nothing to do
+    assert prefill(good, total_q=0) == ops.LAZY_OK
+    assert prefill(good, max_q=0) == ops.LAZY_EINVAL
+    assert prefill(good, q=None) == ops.LAZY_EINVAL
+    assert prefill(good, out=None) == ops.LAZY_EINVAL
+    # a workload that needs a split workspace but gets none
+    big = P(8, 2, 128, 1, 1e4, 0.0, None, 4, 0)
+    assert prefill(big, max_kv=4096) == ops.LAZY_EWORKSPACE
+    assert prefill(big, max_kv=4096, ws=ctypes.c_void_p(0x1004), ws_bytes=1 << 30) == ops.LAZY_EWORKSPACE  # misaligned
+    # decode
+    assert L.lazy_attn_decode(ctypes.byref(good), None, fake, fake, fake, fake, fake, 2, 100, fake, None, None, 0,
+                              None) == ops.LAZY_EINVAL
+    assert L.lazy_attn_decode(ctypes.byref(good), fake, fake, fake, fake, fake, fake, 0, 100, fake, None, None, 0,
+                              None) == ops.LAZY_OK
+    # combine / materialize
+    assert L.lazy_attn_combine(fake, fake, 0, 10, 128, fake, None, None) == ops.LAZY_EINVAL
+    assert L.lazy_attn_combine(fake, fake, 2, 10, 80, fake, None, None) == ops.LAZY_EUNSUPPORTED
+    assert L.lazy_attn_combine(fake, fake, 2, 0, 128, fake, None, None) == ops.LAZY_OK
+    assert L.lazy_materialize_k(ctypes.byref(good), fake, fake, -1, 10, 10, fake, fake, None) == ops.LAZY_EINVAL
+    assert L.lazy_materialize_k(ctypes.byref(good), fake, fake, 0, 10, 10, fake, fake, None) == ops.LAZY_OK
+
+
+def test_workspace_size_matches_split_formula(ops):
+    cfg = ops.Config(32, 8, 128, 5e5, num_splits=4)
+    assert ops.prefill_workspace_size(cfg, 8, 512, 64, 5312) == 4 * 512 * 32 * 130 * 4
+    cfg1 = ops.Config(32, 8, 128, 5e5, num_splits=1)
+    assert ops.prefill_workspace_size(cfg1, 8, 512, 64, 5312) == 0
+    auto = ops.Config(32, 8, 128, 5e5)
+    n = ops.prefill_workspace_size(auto, 8, 512, 64, 5312)
+    assert n % (512 * 32 * 130 * 4) == 0 and n == ops.prefill_workspace_size(auto, 8, 512, 64, 5312)
+    assert ops.decode_workspace_size(ops.Config(32, 8, 128, 5e5, num_splits=3), 64, 16449) == 3 * 64 * 32 * 130 * 4
+    assert ops.decode_workspace_size(auto, 0, 100) == 0
+
+
+def test_strerror_and_version(ops):
+    assert ops.strerror(0) == "success"
+    assert "workspace" in ops.strerror(-3)
+    assert ops.strerror(12345) == "unknown error"
+    assert ops.lib().lazy_attn_version() >= 100
+
+
+def test_binding_rejects_host_tensors(ops):
+    import torch
+
+    cfg = ops.Config(2, 1, 64, 1e4)
+    t = torch.zeros(4, 2, 64, dtype=torch.bfloat16)
+    i = torch.zeros(2, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        ops.prefill(cfg, t, i, i, t, t, torch.zeros(32, dtype=torch.uint8), i, 4, 4)
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ missing")
+def test_validator_under_address_and_ub_sanitizers(tmp_path):
+    """Host validation code built with ASan/UBSan and driven through valid and invalid tables."""
+    drv = tmp_path / "drv.cpp"
+    drv.write_text(r'''
+#include <cstdio>
+#include <vector>
+#include "lazy_attn.h"
+int main() {
+  lazy_attn_params_t p = {4, 2, 64, 1, 1e4f, 0.f, nullptr, 0, 0};
+  std::vector<lazy_chunk_t> c = {{0, 2048, 16, 0, 16, 16}, {4096, 6144, 8, 16, 8, 8}, {8192, 10240, 4, 24, 4, 4}};
+  std::vector<int> cs = {0, 2, 3}, qs = {0, 2, 4}, qp = {24, 24};
+  int64_t bad; const char* why;
+  int rc = lazy_attn_validate(&p, qs.data(), qp.data(), c.data(), cs.data(), 2, 1 << 16, 1 << 16, &bad, &why);
+  if (rc != LAZY_OK) { printf("valid tables rejected: %s\n", why); return 1; }
+  int fails = 0;
+  for (int k = 0; k < 8; ++k) {
+    std::vector<lazy_chunk_t> m = c; std::vector<int> mcs = cs, mqs = qs, mqp = qp;
+    switch (k) {
+      case 0: m[0].len = 0; break;
+      case 1: m[1].pos_offset = -1; break;
+      case 2: m[2].k_offset = 3; break;
+      case 3: m[0].k_stride = 2; break;
+      case 4: m[1].k_offset = (1 << 16) - 8; break;
+      case 5: mcs[1] = 5; break;
+      case 6: mqs[1] = -1; break;
+      case 7: mqp[1] = -3; break;
+    }
+    rc = lazy_attn_validate(&p, mqs.data(), mqp.data(), m.data(), mcs.data(), 2, 1 << 16, 1 << 16, &bad, &why);
+    if (rc != LAZY_EDATA) { printf("case %d not rejected (%d)\n", k, rc); ++fails; }
+  }
+  if (lazy_attn_validate(nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, 0, nullptr, nullptr) != LAZY_EINVAL) ++fails;
+  printf("sanitized validator ok=%d\n", fails == 0);
+  return fails;
+}
+''')
+    exe = tmp_path / "drv"
+    subprocess.run(["g++", "-std=c++17", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-I",
+                    os.path.join(ROOT, "include"), str(drv), os.path.join(B.CSRC, "lazy_attn_validate.cpp"), "-o",
+                    str(exe)], check=True)
+    res = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert "ok=1" in res.stdout
