@@ -109,8 +109,8 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported (the hot path shards by "
-              "request / KV head without communication, see DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: only one GPU is measured; --gpus {args.gpus} is not supported (the hot path would shard "
+              "by request and KV head with no communication)", file=sys.stderr)
         return 2
     rank = int(os.environ.get("RANK", "0"))
 

@@ -21,7 +21,8 @@ ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 CXX = os.environ.get("CXX", shutil.which("g++") or "g++")
 
-# Packed fp32 VALU ops are disabled for every HIP translation unit ("Toolchain").
+# Packed fp32 VALU ops are disabled for every HIP translation unit: some of their forms have produced silently
+# wrong results on this hardware, so the compiler must not form them from scalar or float2 code.
 HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -39,7 +39,7 @@ struct AttnArgs {
 // Packed rows (token, head in group) handled by one prefill workgroup, and keys per decode tile.
 constexpr int kPrefillRowsPerBlock = 128;  // packed rows of a prefill workgroup per row block
 constexpr int kPrefillTileKeys = 64;
-constexpr int kDecodeTileKeys = 128;  // keys a decode workgroup consumes per round (4 waves x 32)
+constexpr int kDecodeTileKeys = 128;  // keys a decode workgroup consumes per step (4 waves x 32)
 constexpr int kDecodeHeadsPerGroup = 16;
 
 hipError_t launch_prefill(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t stream);
