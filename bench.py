@@ -100,8 +100,9 @@ def cpu_baseline(w, flops_per_pass: float, budget_s: float = 12.0):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=500,
+                    help="untimed steps first; the GPU clocks need some tens of ms of load to settle")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode and baseline legs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--copy-probe-mib", type=int, default=0,

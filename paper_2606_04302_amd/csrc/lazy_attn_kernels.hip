@@ -64,6 +64,28 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 }
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+// A value that is the same in every lane of the wave, marked as such.  The compiler cannot prove it for values
+// derived from threadIdx (the wave index) or computed with the vector integer-division expansion; without the mark
+// the chunk-table walk that depends on them runs as divergent vector code, its record loads become vector loads,
+// and their waits drain the vector-memory queue that holds the next tile's prefetched K / V.
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+// Reductions over lane pairs (l, l ^ 32) with v_permlane32_swap (one VALU op, no LDS round trip).  Swapping a
+// register with itself yields x[l % 32] in one result and x[l % 32 + 32] in the other, in every lane, so both
+// lanes of a pair combine the same two values in the same order.
+__device__ __forceinline__ float xor32_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// acc + (lo + hi) of a packed bf16 pair (v_dot2c_f32_bf16 with weights 1): the softmax denominator is summed over
+// the same bf16-rounded probabilities that enter the P V product.
+__device__ __forceinline__ float add_pair(uint32_t pair, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pair), bf16x2{(__bf16)1.0f, (__bf16)1.0f}, acc,
+                                         false);
+}
 
 // theta_t / (2 pi): RoPE frequency of pair t in revolutions per position (original RoPE: base^(-2t/D);
 // RoPE variants pass their own table, Sec. 3.5).
@@ -419,7 +441,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     qpos[rb] = qp0 + tok[rb];
   }
   const int last = min(row0 + BM, nrows) - 1;
-  const int qmin = qp0 + row0 / G, qmax = qp0 + last / G;
+  const int qmin = uniform(qp0 + row0 / G), qmax = uniform(qp0 + last / G);
 
   bf16x8 qf[RB][D / 16];
 #pragma unroll
@@ -504,6 +526,9 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     f32x16 sa[RB][2];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) sa[rb][0] = sa[rb][1] = f32x16{};
+    // Waves raise their issue priority while they feed the matrix cores, so that the MFMA blocks of one wave run
+    // ahead and the other wave's softmax / rotation VALU work fills the gaps.
+    __builtin_amdgcn_s_setprio(1);
     {
       const uint16_t* kl = kb + (lane & 31) * S::KLD;
       u32x4 kv[2][2];
@@ -527,6 +552,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     if (nvalid < kSub || (a.causal && b0 + kSub - 1 > qmin)) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
@@ -539,6 +565,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
             if (!ok) sa[rb][blk][i] = -INFINITY;
           }
     }
+    uint32_t pk[RB][16];  // bf16 pairs of P: block blk, keys 8 (i / 4) + 4 h2 + i % 4 for i = 2 j, 2 j + 1
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       float mx = -INFINITY;
@@ -546,7 +573,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
       for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sa[rb][blk][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = xor32_max(mx);
       // Lazy rescale: the reference max only moves when this tile's max exceeds it by more than kRescaleSlack.
       const float mt = mx * c;
       if (__any(mt > m2[rb] + kRescaleSlack)) {
@@ -558,28 +585,31 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
         m2[rb] = mnew;
       }
       const float muse = m2[rb] == -INFINITY ? 0.f : m2[rb];
-      float ps = 0.f;
+      float ps0 = 0.f, ps1 = 0.f;
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = fast_exp2(fmaf(sa[rb][blk][i], c, -muse));
-          sa[rb][blk][i] = p;
-          ps += p;
+        for (int j = 0; j < 8; ++j) {
+          const uint32_t pp = pack2(fast_exp2(fmaf(sa[rb][blk][2 * j], c, -muse)),
+                                    fast_exp2(fmaf(sa[rb][blk][2 * j + 1], c, -muse)));
+          pk[rb][8 * blk + j] = pp;
+          if (j & 1)
+            ps1 = add_pair(pp, ps1);
+          else
+            ps0 = add_pair(pp, ps0);
         }
-      lsum[rb] += ps;
+      lsum[rb] += ps0 + ps1;
     }
 
     // O^T += V^T P^T: four 16-key steps; each V fragment feeds RB MFMAs (same bounded read-ahead).
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int s2 = 0; s2 < 4; ++s2) {
       bf16x8 pb[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        const f32x16& sv = sa[rb][s2 >> 1];
-        const int bq = 8 * (s2 & 1);
-        pb[rb] = as_bf16x8(u32x4{pack2(sv[bq + 0], sv[bq + 1]), pack2(sv[bq + 2], sv[bq + 3]),
-                                 pack2(sv[bq + 4], sv[bq + 5]), pack2(sv[bq + 6], sv[bq + 7])});
+        const int j0 = 8 * (s2 >> 1) + 4 * (s2 & 1);
+        pb[rb] = as_bf16x8(u32x4{pk[rb][j0], pk[rb][j0 + 1], pk[rb][j0 + 2], pk[rb][j0 + 3]});
       }
       u32x4 vv[D / 32];
 #pragma unroll
@@ -596,6 +626,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
       __builtin_amdgcn_sched_barrier(0);
     }
 
+    __builtin_amdgcn_s_setprio(0);
     if (NBUF == 2) {
       // Base angles two tiles ahead go to the table slot this tile used; the next tile goes to the other buffer.
       if (ROT && have_ahead) prefill_base<D>(sm.csb[parity][0], sm.freq, tid, ahead.cur.pos + ahead.j0);
@@ -608,7 +639,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
 
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const float ltot = lsum[rb] + __shfl_xor(lsum[rb], 32);
+    const float ltot = xor32_sum(lsum[rb]);
     if (!rvalid[rb]) continue;
     const int64_t orow = (int64_t)(qs + tok[rb]) * a.hq + head[rb];
     if (a.splits == 1) {
@@ -733,7 +764,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   __shared__ DecodeSmem<D> sm;
   using S = DecodeSmem<D>;
   constexpr int SP = DecTile<D>::SP;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int split = blockIdx.x;
   const int g = blockIdx.y / a.head_groups, hg = blockIdx.y % a.head_groups;
   const int r = blockIdx.z;
