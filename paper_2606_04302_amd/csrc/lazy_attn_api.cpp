@@ -118,7 +118,7 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
   a.q_tiles = q_tiles;
   a.row_blocks = prefill_row_blocks(p, max_q_len);
   a.head_groups = 1;
-  a.rope_base = p->rope_base;
+  a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   return status(lazy::launch_prefill(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
@@ -161,7 +161,7 @@ int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const 
   a.q_tiles = 1;
   a.row_blocks = 1;
   a.head_groups = hg;
-  a.rope_base = p->rope_base;
+  a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   return status(lazy::launch_decode(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
@@ -237,7 +237,8 @@ int lazy_materialize_k(const lazy_attn_params_t* params, const void* k_pool, con
   if (!k_pool || !chunks || !chunks_out || (total_kv > 0 && !k_out)) return LAZY_EINVAL;
   if (num_records > 65535 || params->num_kv_heads > 65535) return LAZY_EUNSUPPORTED;
   return status(lazy::launch_materialize(static_cast<const uint16_t*>(k_pool), chunks, num_records, max_chunk_len,
-                                         params->num_kv_heads, params->head_dim, params->rope_base,
+                                         params->num_kv_heads, params->head_dim,
+                                         params->inv_freq ? 0.0 : log2((double)params->rope_base),
                                          params->inv_freq, static_cast<uint16_t*>(k_out), chunks_out,
                                          static_cast<hipStream_t>(stream)));
 }

@@ -32,7 +32,7 @@ struct AttnArgs {
   int32_t q_tiles;            // prefill: row tiles per (request, kv head)
   int32_t row_blocks;         // prefill: a workgroup covers 128 * row_blocks packed rows (2 = eight-wave kernel)
   int32_t head_groups;        // decode: ceil(group / 16)
-  float rope_base;
+  double rope_log2_base;      // log2(rope_base), computed on the host (unused with inv_freq)
   float scale_log2;           // softmax scale * log2(e)
 };
 
@@ -47,7 +47,7 @@ hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStre
 hipError_t launch_combine(const float* acc, const float* ml, int splits, int rows, int head_dim, uint16_t* out,
                           float* lse, hipStream_t stream);
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
-                              int max_chunk_len, int hkv, int head_dim, float rope_base, const float* inv_freq,
+                              int max_chunk_len, int hkv, int head_dim, double rope_log2_base, const float* inv_freq,
                               uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t stream);
 
 }  // namespace lazy

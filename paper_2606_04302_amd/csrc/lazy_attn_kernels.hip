@@ -87,10 +87,11 @@ __device__ __forceinline__ float add_pair(uint32_t pair, float acc) {
                                          false);
 }
 
-// theta_t / (2 pi): RoPE frequency of pair t in revolutions per position (original RoPE: base^(-2t/D);
-// RoPE variants pass their own table, Sec. 3.5).
-__device__ __forceinline__ double theta_rev(int t, int d, float base, const float* inv_freq) {
-  const double th = inv_freq ? (double)inv_freq[t] : pow((double)base, -2.0 * (double)t / (double)d);
+// theta_t / (2 pi): RoPE frequency of pair t in revolutions per position (original RoPE: base^(-2t/D), evaluated as
+// exp2(-(2t/D) log2(base)) with log2(base) from the host, far cheaper than a double pow; RoPE variants pass their own
+// table, Sec. 3.5).
+__device__ __forceinline__ double theta_rev(int t, int d, double log2_base, const float* inv_freq) {
+  const double th = inv_freq ? (double)inv_freq[t] : exp2(-2.0 * (double)t / (double)d * log2_base);
   return th * kInvTwoPi;
 }
 
@@ -229,19 +230,29 @@ __device__ __forceinline__ u32x2 tr_read(const uint16_t* p) {
 template <int D>
 __device__ __forceinline__ int cs_idx(int t) { return 2 * t + 8 * (t / (D / 8)); }
 
-// Load 4 query pairs (t0..t0+3 with their partners t0+D/2..) of one query row, rotated at position p, as one
-// 8-element MFMA fragment in virtual order [low t0..t0+3, high t0..t0+3].
+// Four query pairs (t0..t0+3 with their partners t0+D/2..) of one query row, rotated at position p, as one 8-element
+// MFMA fragment in virtual order [low t0..t0+3, high t0..t0+3].  The angles follow the decomposition used for the
+// keys: cos/sin(p theta_t) from the query block
+// base (qb: position 32 (p / 32)) and the per-row delta table (qd: row p % 32), one angle addition per pair.
 template <int D>
-__device__ __forceinline__ bf16x8 q_fragment(const uint16_t* qrow, int t0, int p, const double* freq, bool valid) {
+__device__ __forceinline__ bf16x8 q_fragment_tab(const uint16_t* qrow, int t0, const float* qb, const float* qd,
+                                                 bool valid) {
   if (!valid) return as_bf16x8(u32x4{0, 0, 0, 0});
   const u32x2 lo = *reinterpret_cast<const u32x2*>(qrow + t0);
   const u32x2 hi = *reinterpret_cast<const u32x2*>(qrow + D / 2 + t0);
+  const f32x4 b01 = reinterpret_cast<const f32x4*>(qb + cs_idx<D>(t0))[0];
+  const f32x4 b23 = reinterpret_cast<const f32x4*>(qb + cs_idx<D>(t0))[1];
+  const f32x4 d01 = reinterpret_cast<const f32x4*>(qd + cs_idx<D>(t0))[0];
+  const f32x4 d23 = reinterpret_cast<const f32x4*>(qd + cs_idx<D>(t0))[1];
   float y1[4], y2[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const float x1 = (e & 1) ? bf_hi(lo[e >> 1]) : bf_lo(lo[e >> 1]);
     const float x2 = (e & 1) ? bf_hi(hi[e >> 1]) : bf_lo(hi[e >> 1]);
-    rotate_q_pair(x1, x2, p, freq[t0 + e], y1[e], y2[e]);
+    const f32x4& bq = e < 2 ? b01 : b23;
+    const f32x4& dq = e < 2 ? d01 : d23;
+    const int o2 = 2 * (e & 1);
+    rotate_pair(x1, x2, make_float2(bq[o2], bq[o2 + 1]), make_float2(dq[o2], dq[o2 + 1]), y1[e], y2[e]);
   }
   return as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y2[0], y2[1]), pack2(y2[2], y2[3])});
 }
@@ -268,6 +279,9 @@ __device__ __forceinline__ int xcd_remap(int id, int n) {
   return id < (per << 3) ? (id & 7) * per + (id >> 3) : id;
 }
 
+// Query positions of a workgroup of at most 256 rows span at most 256 consecutive positions: at most 9 blocks of 32.
+constexpr int kQueryBases = 9;
+
 template <int D, int NBUF>
 struct PrefillSmem {
   using S = TileLayout<D>;
@@ -275,6 +289,7 @@ struct PrefillSmem {
   uint16_t v[NBUF][kSub * S::VLD] __attribute__((aligned(16)));
   float csd[kAngleRows * S::CSD_LD] __attribute__((aligned(16)));  // cos/sin(delta theta_t), delta < 32
   float csb[2][2][S::CSW] __attribute__((aligned(16)));            // [tile parity][half]: cos/sin(base theta_t)
+  float qb[kQueryBases][S::CSW] __attribute__((aligned(16)));      // cos/sin(32 a theta_t) for the query blocks
   double freq[D / 2];
 };
 
@@ -301,19 +316,10 @@ struct PLoader {
   float2 cdr[CSD_REGS && ROT ? PP : 1];
   int tid, row, part;
 
-  // Writes the per-row angle table (rows < 32); it is read after the caller's next barrier.
-  __device__ void init(int t, float* csd, const double* freq) {
+  __device__ void init(int t) {
     tid = t;
     row = t / TPR;
     part = t % TPR;
-    if (ROT && row < kAngleRows) {
-      float* cd = csd + row * S::CSD_LD;
-#pragma unroll
-      for (int e = 0; e < PP; ++e) {
-        const int tt = part * PP + e;
-        *reinterpret_cast<float2*>(cd + cs_idx<D>(tt)) = rope_cs(row, freq[tt]);
-      }
-    }
   }
   // With CSD_REGS, after that barrier: keep this thread's per-row constants in registers (the loop writes LDS, so
   // they cannot be re-derived inside it).
@@ -426,7 +432,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   if (row0 >= nrows) return;
   const int qp0 = as_const(a.q_pos0)[r];
 
-  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_base, a.inv_freq);
+  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
   __syncthreads();
 
   const int h2 = lane >> 5;
@@ -443,12 +449,25 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   const int last = min(row0 + BM, nrows) - 1;
   const int qmin = uniform(qp0 + row0 / G), qmax = uniform(qp0 + last / G);
 
+  // Angle tables: per-row deltas cos/sin(delta theta_t), delta < 32 (queries and keys), and the query block bases
+  // cos/sin(32 a theta_t), a = qmin / 32 .. qmax / 32.
+  const int qa0 = qmin / kAngleRows, nqb = qmax / kAngleRows - qa0 + 1;
+  for (int e = tid; e < (kAngleRows + nqb) * (D / 2); e += NT) {
+    const int trow = e / (D / 2), t = e % (D / 2);
+    float* dst = trow < kAngleRows ? sm.csd + trow * S::CSD_LD : sm.qb[trow - kAngleRows];
+    const int p = trow < kAngleRows ? trow : kAngleRows * (qa0 + trow - kAngleRows);
+    *reinterpret_cast<float2*>(dst + cs_idx<D>(t)) = rope_cs(p, sm.freq[t]);
+  }
+  __syncthreads();
+
   bf16x8 qf[RB][D / 16];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const uint16_t* qrow = a.q + ((int64_t)(qs + tok[rb]) * a.hq + head[rb]) * D;
+    const float* qbr = sm.qb[qpos[rb] / kAngleRows - qa0];
+    const float* qdr = sm.csd + (qpos[rb] & (kAngleRows - 1)) * S::CSD_LD;
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s) qf[rb][s] = q_fragment<D>(qrow, 8 * s + 4 * h2, qpos[rb], sm.freq, rvalid[rb]);
+    for (int s = 0; s < D / 16; ++s) qf[rb][s] = q_fragment_tab<D>(qrow, 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
   }
 
   f32x16 o[RB][D / 32];
@@ -463,11 +482,8 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   const float c = a.scale_log2;
 
   PLoader<D, ROT, NT, RB == 2> ld;
-  ld.init(tid, sm.csd, sm.freq);
-  if constexpr (RB == 2) {
-    __syncthreads();
-    ld.load_constants(sm.csd);
-  }
+  ld.init(tid);
+  ld.load_constants(sm.csd);
   TileIter<kSub> it;
   it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
   bool have = it.seek(a.causal, qmax);
@@ -773,7 +789,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int col = lane & 15, kq = lane >> 4;
   const int qpos = as_const(a.q_pos0)[r];
 
-  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_base, a.inv_freq);
+  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
   __syncthreads();
   if (ROT) {
     // Per-row constants cos/sin(delta theta_t), delta < 32: 16 per thread.
@@ -1063,7 +1079,7 @@ template <int D>
 __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint16_t* __restrict__ k_pool,
                                                                       const lazy_chunk_t* __restrict__ in,
                                                                       const lazy_chunk_t* __restrict__ plan,
-                                                                      float base, const float* inv_freq,
+                                                                      double log2_base, const float* inv_freq,
                                                                       uint16_t* __restrict__ k_out) {
   constexpr int PP = D / 8, NV = PP / 8;
   __shared__ double freq[D / 2];
@@ -1072,7 +1088,7 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
   const Rec rc = load_rec(as_const(in) + blockIdx.z);
   const int g = blockIdx.y, j0 = blockIdx.x * kSub;
   if (j0 >= rc.len) return;
-  if (tid < D / 2) freq[tid] = theta_rev(tid, D, base, inv_freq);
+  if (tid < D / 2) freq[tid] = theta_rev(tid, D, log2_base, inv_freq);
   __syncthreads();
   if (tid < D) cs[tid / (D / 2)][tid % (D / 2)] = rope_cs(rc.pos + j0 + kAngleRows * (tid / (D / 2)), freq[tid % (D / 2)]);
   __syncthreads();
@@ -1159,7 +1175,7 @@ hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStre
 }
 
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
-                              int max_chunk_len, int hkv, int head_dim, float rope_base, const float* inv_freq,
+                              int max_chunk_len, int hkv, int head_dim, double rope_log2_base, const float* inv_freq,
                               uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t st) {
   if (num_records <= 0) return hipSuccess;
   hipLaunchKernelGGL(materialize_plan_kernel, dim3(1), dim3(kThreads), 0, st, chunks, num_records, hkv, head_dim,
@@ -1169,10 +1185,10 @@ hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks
   const dim3 grid((max_chunk_len + kSub - 1) / kSub, hkv, num_records);
   if (head_dim == 128)
     hipLaunchKernelGGL(materialize_rotate_kernel<128>, grid, dim3(kThreads), 0, st, k_pool, chunks, chunks_out,
-                       rope_base, inv_freq, k_out);
+                       rope_log2_base, inv_freq, k_out);
   else
     hipLaunchKernelGGL(materialize_rotate_kernel<64>, grid, dim3(kThreads), 0, st, k_pool, chunks, chunks_out,
-                       rope_base, inv_freq, k_out);
+                       rope_log2_base, inv_freq, k_out);
   return hipGetLastError();
 }
 
