@@ -149,16 +149,14 @@ def main() -> int:
     ms = timed(prefill, args.steps, args.warmup)
 
     # The combine kernel alone on the same partials, to isolate the prefill kernel's own duration.
-    splits = ws_bytes // (wp.total_q * wp.num_q_heads * (wp.head_dim + 2) * 4) if ws_bytes else 1
+    rows = wp.total_q * wp.num_q_heads
+    part_o, part_lse = ops.split_views(ws, rows, wp.head_dim)
+    splits = part_o.shape[0] if part_o is not None else 1
     combine_ms = 0.0
     if splits > 1:
-        rows = wp.total_q * wp.num_q_heads
-        wsf = ws.view(torch.float32)
-        acc = wsf[: splits * rows * wp.head_dim].view(splits, rows, wp.head_dim)
-        ml = wsf[splits * rows * wp.head_dim: splits * rows * (wp.head_dim + 2)].view(splits, rows, 2)
         out2 = torch.empty((rows, wp.head_dim), dtype=torch.bfloat16, device=dev)
         lse2 = torch.empty(rows, dtype=torch.float32, device=dev)
-        combine_ms = timed(lambda: ops.combine(acc, ml, out=out2, lse=lse2), args.steps, args.warmup)
+        combine_ms = timed(lambda: ops.combine(part_o, part_lse, out=out2, lse=lse2), args.steps, args.warmup)
     kernel_ms = ms - combine_ms
 
     # No-rotation diagnostic: the same kernel with K rotation compiled out, over the unrotated store.
@@ -266,7 +264,7 @@ def main() -> int:
             "hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
             "logical_mb": round(dbytes / 1e6, 1),
             "unique_kv_mb": round(A.unique_kv_bytes(wd) / 1e6, 1),
-            "splits": int(wsd_bytes // (wd.batch * wd.num_q_heads * (wd.head_dim + 2) * 4)) if wsd_bytes else 1,
+            "splits": int(wsd_bytes // (wd.batch * wd.num_q_heads * (2 * wd.head_dim + 4))) if wsd_bytes else 1,
             "no_rotation_ms": round(dnorot, 5),
             "rotation_overhead": round(dms / dnorot - 1.0, 4),
             "materialize_ms": round(dmat, 5),

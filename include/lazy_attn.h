@@ -122,15 +122,16 @@ LAZY_API int lazy_attn_decode(const lazy_attn_params_t* params, const void* q, c
 LAZY_API size_t lazy_attn_decode_workspace_size(const lazy_attn_params_t* params, int32_t batch, int32_t max_kv_len);
 
 /*
- * Split-KV merge (standard log-sum-exp combination of partial softmax states over disjoint key sets):
- * with M = max_s m[s][row], w_s = exp(m[s][row] - M):
- *     out[row] = sum_s w_s acc[s][row][:] / sum_s w_s l[s][row],   lse[row] = M + ln(sum_s w_s l[s][row]).
- *   part_acc [splits][rows][D] fp32, part_ml [splits][rows][2] fp32 holding (m, l) with m the natural-log-domain
- *   running max of the scaled scores (-inf for an empty split, then l = 0 and acc = 0).
- *   out [rows][D] bf16; lse [rows] fp32 or NULL.  Rows whose every split is empty get out = 0, lse = -inf.
+ * Split-KV merge (standard log-sum-exp combination of partial softmax results over disjoint key sets): each split s
+ * holds its own normalised output o[s][row] and the log-sum-exp lse[s][row] of its scaled scores (natural log);
+ * with M = max_s lse[s][row] and w_s = exp(lse[s][row] - M):
+ *     out[row] = sum_s w_s o[s][row][:] / sum_s w_s,   lse[row] = M + ln(sum_s w_s).
+ *   part_o [splits][rows][D] bf16, part_lse [splits][rows] fp32 (-inf for a split that saw no key; its o is
+ *   ignored).  out [rows][D] bf16; lse [rows] fp32 or NULL.  Rows whose every split is empty get out = 0,
+ *   lse = -inf.  The prefill / decode workspaces hold exactly these two arrays (part_o first, then part_lse).
  */
-LAZY_API int lazy_attn_combine(const float* part_acc, const float* part_ml, int32_t splits, int32_t rows, int32_t head_dim,
-                      void* out, float* lse, void* stream);
+LAZY_API int lazy_attn_combine(const void* part_o, const float* part_lse, int32_t splits, int32_t rows,
+                               int32_t head_dim, void* out, float* lse, void* stream);
 
 /*
  * Materialise-then-attend baseline, step 1 (the re-encoding copy that LazyAttention avoids; Block-Attention's

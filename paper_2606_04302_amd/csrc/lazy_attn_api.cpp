@@ -71,9 +71,11 @@ int decode_splits(const lazy_attn_params_t* p, int32_t batch, int32_t max_kv_len
   return s < 1 ? 1 : (int)s;
 }
 
+// Split-KV workspace: bf16 normalised partial outputs [splits][rows][d], then fp32 partial lse [splits][rows]
+// (16-byte aligned because d is a multiple of 8).
 size_t split_workspace(int splits, int64_t rows, int d) {
   if (splits <= 1) return 0;
-  return (size_t)splits * (size_t)rows * (size_t)(d + 2) * sizeof(float);
+  return (size_t)splits * (size_t)rows * ((size_t)d * sizeof(uint16_t) + sizeof(float));
 }
 
 int status(hipError_t e) { return e == hipSuccess ? LAZY_OK : LAZY_EHIP; }
@@ -105,8 +107,9 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
   a.chunk_start = chunk_start;
   a.out = static_cast<uint16_t*>(out);
   a.lse = lse;
-  a.ws_acc = need ? static_cast<float*>(workspace) : nullptr;
-  a.ws_ml = need ? static_cast<float*>(workspace) + (size_t)splits * rows * p->head_dim : nullptr;
+  a.ws_o = need ? static_cast<uint16_t*>(workspace) : nullptr;
+  a.ws_lse = need ? reinterpret_cast<float*>(static_cast<uint16_t*>(workspace) + (size_t)splits * rows * p->head_dim)
+                  : nullptr;
   a.inv_freq = p->inv_freq;
   a.batch = batch;
   a.total_q = total_q;
@@ -148,8 +151,9 @@ int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const 
   a.chunk_start = chunk_start;
   a.out = static_cast<uint16_t*>(out);
   a.lse = lse;
-  a.ws_acc = need ? static_cast<float*>(workspace) : nullptr;
-  a.ws_ml = need ? static_cast<float*>(workspace) + (size_t)splits * rows * p->head_dim : nullptr;
+  a.ws_o = need ? static_cast<uint16_t*>(workspace) : nullptr;
+  a.ws_lse = need ? reinterpret_cast<float*>(static_cast<uint16_t*>(workspace) + (size_t)splits * rows * p->head_dim)
+                  : nullptr;
   a.inv_freq = p->inv_freq;
   a.batch = batch;
   a.total_q = batch;
@@ -217,14 +221,14 @@ int lazy_plain_attn_decode(const lazy_attn_params_t* params, const void* q, cons
                     workspace, workspace_bytes, stream);
 }
 
-int lazy_attn_combine(const float* part_acc, const float* part_ml, int32_t splits, int32_t rows, int32_t head_dim,
+int lazy_attn_combine(const void* part_o, const float* part_lse, int32_t splits, int32_t rows, int32_t head_dim,
                       void* out, float* lse, void* stream) {
   if (head_dim != 64 && head_dim != 128) return LAZY_EUNSUPPORTED;
   if (splits <= 0 || rows < 0) return LAZY_EINVAL;
   if (rows == 0) return LAZY_OK;
-  if (!part_acc || !part_ml || !out || ((uintptr_t)part_acc & 15u)) return LAZY_EINVAL;
-  return status(lazy::launch_combine(part_acc, part_ml, splits, rows, head_dim, static_cast<uint16_t*>(out), lse,
-                                     static_cast<hipStream_t>(stream)));
+  if (!part_o || !part_lse || !out || ((uintptr_t)part_o & 15u)) return LAZY_EINVAL;
+  return status(lazy::launch_combine(static_cast<const uint16_t*>(part_o), part_lse, splits, rows, head_dim,
+                                     static_cast<uint16_t*>(out), lse, static_cast<hipStream_t>(stream)));
 }
 
 int lazy_materialize_k(const lazy_attn_params_t* params, const void* k_pool, const lazy_chunk_t* chunks,

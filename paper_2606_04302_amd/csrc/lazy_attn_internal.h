@@ -19,8 +19,8 @@ struct AttnArgs {
   const int32_t* chunk_start; // [batch+1]
   uint16_t* out;              // [total_q][hq][D] bf16 bits
   float* lse;                 // [total_q][hq] or null
-  float* ws_acc;              // [splits][total_q*hq][D] fp32, null when splits == 1
-  float* ws_ml;               // [splits][total_q*hq][2] fp32 (m, l), null when splits == 1
+  uint16_t* ws_o;             // [splits][total_q*hq][D] bf16 normalised partial outputs, null when splits == 1
+  float* ws_lse;              // [splits][total_q*hq] fp32 partial log-sum-exp, null when splits == 1
   const float* inv_freq;      // [D/2] or null
   int32_t batch;
   int32_t total_q;
@@ -44,8 +44,8 @@ constexpr int kDecodeHeadsPerGroup = 16;
 
 hipError_t launch_prefill(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t stream);
 hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t stream);
-hipError_t launch_combine(const float* acc, const float* ml, int splits, int rows, int head_dim, uint16_t* out,
-                          float* lse, hipStream_t stream);
+hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int splits, int rows, int head_dim,
+                          uint16_t* out, float* lse, hipStream_t stream);
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
                               int max_chunk_len, int hkv, int head_dim, double rope_log2_base, const float* inv_freq,
                               uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t stream);

@@ -657,36 +657,21 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   for (int rb = 0; rb < RB; ++rb) {
     const float ltot = xor32_sum(lsum[rb]);
     if (!rvalid[rb]) continue;
+    // Normalised output and log-sum-exp: the final result, or with several splits this split's partial result.
     const int64_t orow = (int64_t)(qs + tok[rb]) * a.hq + head[rb];
-    if (a.splits == 1) {
-      const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
-      uint16_t* dst = a.out + orow * D;
+    const int64_t wrow = (int64_t)split * a.total_q * a.hq + orow;
+    uint16_t* dst = a.splits == 1 ? a.out + orow * D : a.ws_o + wrow * D;
+    float* lse_dst = a.splits == 1 ? (a.lse ? a.lse + orow : nullptr) : a.ws_lse + wrow;
+    const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db)
+    for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const int dim = 32 * db + 8 * q4 + 4 * h2;
-          *reinterpret_cast<u32x2*>(dst + dim) =
-              u32x2{pack2(o[rb][db][4 * q4] * inv, o[rb][db][4 * q4 + 1] * inv),
-                    pack2(o[rb][db][4 * q4 + 2] * inv, o[rb][db][4 * q4 + 3] * inv)};
-        }
-      if (a.lse && h2 == 0) a.lse[orow] = ltot > 0.f ? (m2[rb] + log2f(ltot)) * kLn2 : -INFINITY;
-    } else {
-      const int64_t wrow = (int64_t)split * a.total_q * a.hq + orow;
-      float* dst = a.ws_acc + wrow * D;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const int dim = 32 * db + 8 * q4 + 4 * h2;
-          *reinterpret_cast<f32x4*>(dst + dim) =
-              f32x4{o[rb][db][4 * q4], o[rb][db][4 * q4 + 1], o[rb][db][4 * q4 + 2], o[rb][db][4 * q4 + 3]};
-        }
-      if (h2 == 0) {
-        a.ws_ml[2 * wrow] = m2[rb] * kLn2;
-        a.ws_ml[2 * wrow + 1] = ltot;
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int dim = 32 * db + 8 * q4 + 4 * h2;
+        *reinterpret_cast<u32x2*>(dst + dim) = u32x2{pack2(o[rb][db][4 * q4] * inv, o[rb][db][4 * q4 + 1] * inv),
+                                                     pack2(o[rb][db][4 * q4 + 2] * inv, o[rb][db][4 * q4 + 3] * inv)};
       }
-    }
+    if (lse_dst && h2 == 0) *lse_dst = ltot > 0.f ? (m2[rb] + log2f(ltot)) * kLn2 : -INFINITY;
   }
 }
 
@@ -992,54 +977,50 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       }
     }
     const int hh = g * G + kDecodeHeadsPerGroup * hg + hc;
+    // Normalised output and log-sum-exp: the final result, or with several splits this split's partial result.
     const int64_t orow = (int64_t)r * a.hq + hh;
-    if (a.splits == 1) {
-      const float inv = l > 0.f ? 1.f / l : 0.f;
-      *reinterpret_cast<u32x2*>(a.out + orow * D + 4 * d4) =
-          u32x2{pack2(acc[0] * inv, acc[1] * inv), pack2(acc[2] * inv, acc[3] * inv)};
-      if (a.lse && d4 == 0) a.lse[orow] = l > 0.f ? (mmax + log2f(l)) * kLn2 : -INFINITY;
-    } else {
-      const int64_t wrow = (int64_t)split * a.total_q * a.hq + orow;
-      *reinterpret_cast<f32x4*>(a.ws_acc + wrow * D + 4 * d4) = acc;
-      if (d4 == 0) {
-        a.ws_ml[2 * wrow] = mmax * kLn2;
-        a.ws_ml[2 * wrow + 1] = l;
-      }
-    }
+    const int64_t wrow = (int64_t)split * a.total_q * a.hq + orow;
+    uint16_t* dst = a.splits == 1 ? a.out + orow * D : a.ws_o + wrow * D;
+    float* lse_dst = a.splits == 1 ? (a.lse ? a.lse + orow : nullptr) : a.ws_lse + wrow;
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    *reinterpret_cast<u32x2*>(dst + 4 * d4) = u32x2{pack2(acc[0] * inv, acc[1] * inv), pack2(acc[2] * inv, acc[3] * inv)};
+    if (lse_dst && d4 == 0) *lse_dst = l > 0.f ? (mmax + log2f(l)) * kLn2 : -INFINITY;
   }
 }
 
 // ---------------------------------------------------------------------------------------------------------------
 // Split-KV combine: out = sum_s e^{m_s - M} acc_s / sum_s e^{m_s - M} l_s.  D/4 threads per row, 4 dims each.
 // ---------------------------------------------------------------------------------------------------------------
+// Split-KV merge: per row, the splits' normalised outputs weighted by exp(lse_s - max lse).  One row per D / 8
+// threads, 16-byte loads of bf16 partial rows.
 template <int D>
-__global__ __launch_bounds__(kThreads) void combine_kernel(const float* __restrict__ acc,
-                                                           const float* __restrict__ ml, int splits, int rows,
+__global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __restrict__ part_o,
+                                                           const float* __restrict__ part_lse, int splits, int rows,
                                                            uint16_t* __restrict__ out, float* __restrict__ lse) {
-  constexpr int TPR = D / 4;
+  constexpr int TPR = D / 8;
   const int row = blockIdx.x * (kThreads / TPR) + threadIdx.x / TPR;
-  const int d4 = threadIdx.x % TPR;
+  const int d8 = threadIdx.x % TPR;
   if (row >= rows) return;
   float mmax = -INFINITY;
-  for (int s = 0; s < splits; ++s) mmax = fmaxf(mmax, ml[2 * ((int64_t)s * rows + row)]);
-  float l = 0.f;
-  f32x4 sum = f32x4{};
+  for (int s = 0; s < splits; ++s) mmax = fmaxf(mmax, part_lse[(int64_t)s * rows + row]);
+  float den = 0.f, sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (mmax != -INFINITY) {
     for (int s = 0; s < splits; ++s) {
       const int64_t w = (int64_t)s * rows + row;
-      const float m = ml[2 * w];
-      if (m == -INFINITY) continue;
-      const float sc = expf(m - mmax);
-      l = fmaf(ml[2 * w + 1], sc, l);
-      const f32x4 v = *reinterpret_cast<const f32x4*>(acc + w * D + 4 * d4);
+      const float ls = part_lse[w];
+      if (ls == -INFINITY) continue;
+      const float sc = expf(ls - mmax);
+      den += sc;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(part_o + w * D + 8 * d8);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sum[e] = fmaf(v[e], sc, sum[e]);
+      for (int e = 0; e < 8; ++e) sum[e] = fmaf((e & 1) ? bf_hi(v[e >> 1]) : bf_lo(v[e >> 1]), sc, sum[e]);
     }
   }
-  const float inv = l > 0.f ? 1.f / l : 0.f;
-  *reinterpret_cast<u32x2*>(out + (int64_t)row * D + 4 * d4) =
-      u32x2{pack2(sum[0] * inv, sum[1] * inv), pack2(sum[2] * inv, sum[3] * inv)};
-  if (lse && d4 == 0) lse[row] = l > 0.f ? mmax + logf(l) : -INFINITY;
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  *reinterpret_cast<u32x4*>(out + (int64_t)row * D + 8 * d8) =
+      u32x4{pack2(sum[0] * inv, sum[1] * inv), pack2(sum[2] * inv, sum[3] * inv), pack2(sum[4] * inv, sum[5] * inv),
+            pack2(sum[6] * inv, sum[7] * inv)};
+  if (lse && d8 == 0) lse[row] = den > 0.f ? mmax + logf(den) : -INFINITY;
 }
 
 // ---------------------------------------------------------------------------------------------------------------
@@ -1142,15 +1123,15 @@ hipError_t decode_d(const AttnArgs& a, hipStream_t st) {
 
 }  // namespace
 
-hipError_t launch_combine(const float* acc, const float* ml, int splits, int rows, int head_dim, uint16_t* out,
-                          float* lse, hipStream_t st) {
+hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int splits, int rows, int head_dim,
+                          uint16_t* out, float* lse, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  const int per_block = kThreads / (head_dim / 4);
+  const int per_block = kThreads / (head_dim / 8);
   const dim3 grid((rows + per_block - 1) / per_block);
   if (head_dim == 128)
-    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kThreads), 0, st, acc, ml, splits, rows, out, lse);
+    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, out, lse);
   else
-    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(kThreads), 0, st, acc, ml, splits, rows, out, lse);
+    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, out, lse);
   return hipGetLastError();
 }
 
@@ -1161,7 +1142,7 @@ hipError_t launch_prefill(const AttnArgs& a, int head_dim, bool rotate_k, hipStr
   else
     e = rotate_k ? prefill_d<64, true>(a, st) : prefill_d<64, false>(a, st);
   if (e != hipSuccess || a.splits == 1) return e;
-  return launch_combine(a.ws_acc, a.ws_ml, a.splits, a.total_q * a.hq, head_dim, a.out, a.lse, st);
+  return launch_combine(a.ws_o, a.ws_lse, a.splits, a.total_q * a.hq, head_dim, a.out, a.lse, st);
 }
 
 hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t st) {
@@ -1171,7 +1152,7 @@ hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStre
   else
     e = rotate_k ? decode_d<64, true>(a, st) : decode_d<64, false>(a, st);
   if (e != hipSuccess || a.splits == 1) return e;
-  return launch_combine(a.ws_acc, a.ws_ml, a.splits, a.total_q * a.hq, head_dim, a.out, a.lse, st);
+  return launch_combine(a.ws_o, a.ws_lse, a.splits, a.total_q * a.hq, head_dim, a.out, a.lse, st);
 }
 
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,

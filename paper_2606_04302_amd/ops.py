@@ -223,20 +223,33 @@ def decode(cfg: Config, q, q_pos, k_pool, v_pool, chunks, chunk_start, max_kv_le
     return out, lse
 
 
-def combine(part_acc, part_ml, out=None, lse=None, stream=None):
-    """lazy_attn_combine: part_acc [S, rows, D] fp32, part_ml [S, rows, 2] fp32 -> out [rows, D] bf16, lse."""
-    _dev(part_acc, torch.float32, "part_acc")
-    _dev(part_ml, torch.float32, "part_ml")
-    s, rows, d = part_acc.shape
-    _need(part_ml.shape == (s, rows, 2), "part_ml must be [S, rows, 2]")
+def combine(part_o, part_lse, out=None, lse=None, stream=None):
+    """lazy_attn_combine: part_o [S, rows, D] bf16 (normalised partial outputs), part_lse [S, rows] fp32
+    -> out [rows, D] bf16, lse [rows] fp32 (optional)."""
+    _dev(part_o, torch.bfloat16, "part_o")
+    _dev(part_lse, torch.float32, "part_lse")
+    s, rows, d = part_o.shape
+    _need(part_lse.shape == (s, rows), "part_lse must be [S, rows]")
     if out is None:
-        out = torch.empty((rows, d), dtype=torch.bfloat16, device=part_acc.device)
+        out = torch.empty((rows, d), dtype=torch.bfloat16, device=part_o.device)
     _dev(out, torch.bfloat16, "out")
     if lse is not None:
         _dev(lse, torch.float32, "lse")
-    _check(lib().lazy_attn_combine(part_acc.data_ptr(), part_ml.data_ptr(), s, rows, d, out.data_ptr(), _ptr(lse),
+    _check(lib().lazy_attn_combine(part_o.data_ptr(), part_lse.data_ptr(), s, rows, d, out.data_ptr(), _ptr(lse),
                                    _stream(stream)), "lazy_attn_combine")
     return out, lse
+
+
+def split_views(workspace, rows: int, head_dim: int):
+    """The split-KV partial results inside a prefill / decode workspace: (part_o [S, rows, D] bf16,
+    part_lse [S, rows] fp32), S = the number of splits the workspace was sized for (0 if it is empty)."""
+    per = rows * (2 * head_dim + 4)
+    s = workspace.numel() // per if per else 0
+    if s <= 1:
+        return None, None
+    po = workspace[: s * rows * head_dim * 2].view(torch.bfloat16).view(s, rows, head_dim)
+    pl = workspace[s * rows * head_dim * 2: s * per].view(torch.float32).view(s, rows)
+    return po, pl
 
 
 def materialize_k(cfg: Config, k_pool, chunks, max_chunk_len: int, total_kv: int, k_out=None, chunks_out=None,

@@ -165,13 +165,14 @@ def test_scalar_argument_errors_return_before_any_launch(ops):
 
 def test_workspace_size_matches_split_formula(ops):
     cfg = ops.Config(32, 8, 128, 5e5, num_splits=4)
-    assert ops.prefill_workspace_size(cfg, 8, 512, 64, 5312) == 4 * 512 * 32 * 130 * 4
+    # per split and row: the bf16 normalised output (2 D bytes) and its fp32 log-sum-exp
+    assert ops.prefill_workspace_size(cfg, 8, 512, 64, 5312) == 4 * 512 * 32 * (2 * 128 + 4)
     cfg1 = ops.Config(32, 8, 128, 5e5, num_splits=1)
     assert ops.prefill_workspace_size(cfg1, 8, 512, 64, 5312) == 0
     auto = ops.Config(32, 8, 128, 5e5)
     n = ops.prefill_workspace_size(auto, 8, 512, 64, 5312)
-    assert n % (512 * 32 * 130 * 4) == 0 and n == ops.prefill_workspace_size(auto, 8, 512, 64, 5312)
-    assert ops.decode_workspace_size(ops.Config(32, 8, 128, 5e5, num_splits=3), 64, 16449) == 3 * 64 * 32 * 130 * 4
+    assert n % (512 * 32 * (2 * 128 + 4)) == 0 and n == ops.prefill_workspace_size(auto, 8, 512, 64, 5312)
+    assert ops.decode_workspace_size(ops.Config(32, 8, 128, 5e5, num_splits=3), 64, 16449) == 3 * 64 * 32 * (2 * 128 + 4)
     assert ops.decode_workspace_size(auto, 0, 100) == 0
 
 

@@ -194,10 +194,14 @@ def test_combine_entry_point_matches_oracle_merge():
     l = np.where(np.isfinite(m), rng.uniform(1, 50, size=(s, rows)), 0.0)
     acc = np.where(np.isfinite(m)[..., None], rng.normal(size=(s, rows, d)), 0.0)
     ref_o, ref_l = O.merge_partials(m, l, acc)
-    ml = torch.tensor(np.stack([m, l], -1), dtype=torch.float32, device="cuda")
-    ta = torch.tensor(acc, dtype=torch.float32, device="cuda")
+    # the kernels' partial format: per split the normalised output (bf16) and its log-sum-exp m + ln(l)
+    fin = np.isfinite(m)
+    part_o = np.where(fin[..., None], acc / np.where(fin, l, 1.0)[..., None], 0.0)
+    part_lse = np.where(fin, m + np.log(np.where(fin, l, 1.0)), -np.inf)
+    po = torch.tensor(part_o, dtype=torch.float32, device="cuda").to(torch.bfloat16)
+    pl = torch.tensor(part_lse, dtype=torch.float32, device="cuda")
     lse = torch.empty(rows, dtype=torch.float32, device="cuda")
-    out, _ = ops.combine(ta, ml, lse=lse)
+    out, _ = ops.combine(po, pl, lse=lse)
     torch.cuda.synchronize()
     assert_close(out, lse, ref_o, ref_l, tag="combine")
 
