@@ -68,6 +68,35 @@ def timed(fn, steps: int, warmup: int):
     return start.elapsed_time(end) / steps
 
 
+def timed_graph(fn, reps: int, inner: int = 20):
+    """Average ms per call of a short GPU call whose host-side launch cost would otherwise dominate: ``inner``
+    calls captured in one HIP graph, the graph replayed ``reps`` times between HIP events."""
+    import torch
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(3):
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(inner):
+            fn()
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        g.replay()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / (reps * inner)
+
+
 def cpu_baseline(w, flops_per_pass: float, budget_s: float = 12.0):
     """The fp64 oracle on the host cores, whole passes over the same batch until ``budget_s`` has elapsed."""
     from oracle import lazy_oracle as O
@@ -97,6 +126,156 @@ def cpu_baseline(w, flops_per_pass: float, budget_s: float = 12.0):
     }
 
 
+def other_configs(dev, steps: int, warmup: int, log):
+    """Per-configuration figures beyond the headline, lazy vs materialise-then-attend:
+    - icl: many-shot ICL batch (B=4, 32/8 heads, D=128, a shared pool of 128 x 256-token exemplars permuted per
+      request, 256-token causal query at 32,768), its prefill, then 128 decode steps (the query's own chunk grows
+      by one token per step, one query per request at the newest position).  The baseline materialises the
+      rotated keys once (at the final lengths, so the appended keys are included) and runs the plain kernels.
+    - varlen_rag: 16 requests, 28/4 heads, D=128, base 1e6, 8-24 chunks of U[128, 2048] tokens per request drawn
+      Zipf(2.1) without replacement from a 200-chunk pool, queries of U[32, 256] tokens."""
+    import torch
+
+    from paper_2606_04302_amd import accounting as A
+    from paper_2606_04302_amd import ops
+    from paper_2606_04302_amd import workloads as W
+
+    res = {}
+
+    def materialized(w, dw, chunks_np):
+        total_kv = int(chunks_np["len"].astype(np.int64).sum())
+        ch = ops.chunks_tensor(chunks_np, dev)
+        k_out = torch.empty(dw.cfg.num_kv_heads * total_kv * dw.cfg.head_dim, dtype=torch.bfloat16, device=dev)
+        ch_out = torch.empty_like(ch)
+        mx = int(chunks_np["len"].max())
+        fn = lambda: ops.materialize_k(dw.cfg, dw.pool, ch, mx, total_kv, k_out=k_out, chunks_out=ch_out)
+        return fn, k_out, ch_out
+
+    # ---- icl prefill + 128 decode steps ----
+    log("icl workload: generating")
+    w = W.icl_prefill(seed=3)
+    dw = ops.upload(w, dev)
+    cfg = dw.cfg
+    flops = A.useful_flops(w)
+    ws = torch.empty(max(16, ops.prefill_workspace_size(cfg, w.batch, w.total_q, w.max_q_len, w.max_kv_len)),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty_like(dw.q)
+    pre = lambda: ops.prefill(cfg, dw.q, dw.q_start, dw.q_pos0, dw.pool, dw.pool, dw.chunks, dw.chunk_start,
+                              w.max_q_len, w.max_kv_len, out=out, workspace=ws)
+    log("icl: timing prefill")
+    pre_ms = timed(pre, steps, warmup)
+
+    n_steps = int(w.meta["decode_steps"])
+    own = [int(w.chunk_start[r + 1]) - 1 for r in range(w.batch)]
+    tables, dec_flops, dec_bytes, max_kv = [], 0, 0, 0
+    hq, hkv, d = w.num_q_heads, w.num_kv_heads, w.head_dim
+    for s in range(n_steps):
+        ch = w.chunks.copy()
+        qpos = np.empty(w.batch, dtype=np.int32)
+        for r, i in enumerate(own):
+            ch[i]["len"] = int(w.q_lens[r]) + s + 1
+            qpos[r] = int(ch[i]["pos_offset"]) + int(ch[i]["len"]) - 1
+        lens = [int(ch[int(w.chunk_start[r]):int(w.chunk_start[r + 1])]["len"].astype(np.int64).sum())
+                for r in range(w.batch)]
+        max_kv = max(max_kv, max(lens))
+        dec_flops += 4 * d * hq * sum(lens)
+        dec_bytes += sum(lens) * hkv * d * 2 * 2 + 2 * w.batch * hq * d * 2
+        tables.append((ch, ops.chunks_tensor(ch, dev), torch.from_numpy(qpos).to(dev)))
+    rng = np.random.default_rng(33)
+    qd = ops.bf16_tensor(W.bf16_round(rng.standard_normal((w.batch, hq, d), dtype=np.float32)), dev)
+    outd = torch.empty_like(qd)
+    wsd = torch.empty(max(16, ops.decode_workspace_size(cfg, w.batch, max_kv)), dtype=torch.uint8, device=dev)
+
+    def decode_all(kp=None, plain_tables=None):
+        for s, (_, ch, qp) in enumerate(tables):
+            if plain_tables is None:
+                ops.decode(cfg, qd, qp, dw.pool, dw.pool, ch, dw.chunk_start, max_kv, out=outd, workspace=wsd)
+            else:
+                ops.decode(cfg, qd, qp, kp, dw.pool, plain_tables[s], dw.chunk_start, max_kv, out=outd,
+                           workspace=wsd, plain=True)
+
+    reps = max(3, steps // 40)
+    log("icl: timing 128 decode steps")
+    dec_ms = timed(decode_all, reps, 2)
+
+    # Baseline: keys materialised once at their final lengths; per-step tables point into the copy.
+    final = tables[-1][0]
+    mat_fn, k_mat, ch_mat = materialized(w, dw, final)
+    mat_fn()
+    torch.cuda.synchronize()
+    mat_np = ops.chunks_from_tensor(ch_mat)
+    pre_tab = mat_np.copy()
+    for r, i in enumerate(own):
+        pre_tab[i]["len"] = int(w.chunks[i]["len"])
+    pre_tab_t = ops.chunks_tensor(pre_tab, dev)
+    plain_tabs = []
+    for ch, _, _ in tables:
+        t = mat_np.copy()
+        for i in own:
+            t[i]["len"] = int(ch[i]["len"])
+        plain_tabs.append(ops.chunks_tensor(t, dev))
+    log("icl: timing the baseline")
+    mat_ms = timed(mat_fn, max(5, steps // 5), 2)
+    plain_pre_ms = timed(lambda: ops.prefill(cfg, dw.q, dw.q_start, dw.q_pos0, k_mat, dw.pool, pre_tab_t,
+                                             dw.chunk_start, w.max_q_len, w.max_kv_len, out=out, workspace=ws,
+                                             plain=True), steps, warmup)
+    plain_dec_ms = timed(lambda: decode_all(k_mat, plain_tabs), reps, 2)
+    lazy_total = pre_ms + dec_ms
+    base_total = mat_ms + plain_pre_ms + plain_dec_ms
+    res["icl"] = {
+        "workload": "icl: batch 4, 32/8 heads, head_dim 128, base 5e5, 128 x 256-token exemplars (shared pool, "
+                    "permuted per request), 256-token query at 32,768, then 128 decode steps",
+        "prefill_ms": round(pre_ms, 5),
+        "prefill_tflops": round(flops / (pre_ms * 1e-3) / 1e12, 3),
+        "prefill_mfma_frac": round(flops / (pre_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 5),
+        "decode_128_steps_ms": round(dec_ms, 4),
+        "decode_ms_per_step": round(dec_ms / n_steps, 5),
+        "decode_logical_hbm_gbps": round(dec_bytes / (dec_ms * 1e-3) / 1e9, 1),
+        "decode_logical_hbm_frac": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "decode_logical_gb": round(dec_bytes / 1e9, 3),
+        "unique_kv_mb": round(A.unique_kv_bytes(w) / 1e6, 1),
+        "lazy_prefill_plus_decode_ms": round(lazy_total, 4),
+        "materialize_ms": round(mat_ms, 5),
+        "plain_prefill_ms": round(plain_pre_ms, 5),
+        "plain_decode_128_steps_ms": round(plain_dec_ms, 4),
+        "materialize_then_attend_ms": round(base_total, 4),
+        "speedup_vs_materialize": round(base_total / lazy_total, 3),
+    }
+    del k_mat, dw, ws, wsd
+
+    # ---- varlen_rag prefill ----
+    log("varlen_rag workload: generating")
+    w = W.varlen_rag(seed=4)
+    dw = ops.upload(w, dev)
+    cfg = dw.cfg
+    flops = A.useful_flops(w)
+    ws = torch.empty(max(16, ops.prefill_workspace_size(cfg, w.batch, w.total_q, w.max_q_len, w.max_kv_len)),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty_like(dw.q)
+    log("varlen_rag: timing")
+    ms = timed(lambda: ops.prefill(cfg, dw.q, dw.q_start, dw.q_pos0, dw.pool, dw.pool, dw.chunks, dw.chunk_start,
+                                   w.max_q_len, w.max_kv_len, out=out, workspace=ws), steps, warmup)
+    mat_fn, k_mat, ch_mat = materialized(w, dw, w.chunks)
+    mat_ms = timed(mat_fn, max(5, steps // 5), 2)
+    plain_ms = timed(lambda: ops.prefill(cfg, dw.q, dw.q_start, dw.q_pos0, k_mat, dw.pool, ch_mat, dw.chunk_start,
+                                         w.max_q_len, w.max_kv_len, out=out, workspace=ws, plain=True), steps, warmup)
+    res["varlen_rag"] = {
+        "workload": "varlen_rag: batch 16, 28/4 heads, head_dim 128, base 1e6, 8-24 chunks of U[128, 2048] tokens "
+                    "per request, Zipf(2.1) reuse over a 200-chunk pool, U[32, 256]-token queries",
+        "prefill_ms": round(ms, 5),
+        "useful_gflop": round(flops / 1e9, 3),
+        "tflops": round(flops / (ms * 1e-3) / 1e12, 3),
+        "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 5),
+        "logical_kv_mb": round(A.logical_kv_bytes(w) / 1e6, 1),
+        "unique_kv_mb": round(A.unique_kv_bytes(w) / 1e6, 1),
+        "materialize_ms": round(mat_ms, 5),
+        "plain_prefill_ms": round(plain_ms, 5),
+        "materialize_then_attend_ms": round(mat_ms + plain_ms, 5),
+        "speedup_vs_materialize": round((mat_ms + plain_ms) / ms, 3),
+    }
+    return res
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -105,6 +284,7 @@ def main() -> int:
                     help="untimed steps first; the GPU clocks need some tens of ms of load to settle")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode and baseline legs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-other", action="store_true", help="skip the ICL and variable-length RAG configurations")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (reference kernel for HBM counters)")
     args = ap.parse_args()
@@ -156,7 +336,8 @@ def main() -> int:
     if splits > 1:
         out2 = torch.empty((rows, wp.head_dim), dtype=torch.bfloat16, device=dev)
         lse2 = torch.empty(rows, dtype=torch.float32, device=dev)
-        combine_ms = timed(lambda: ops.combine(part_o, part_lse, out=out2, lse=lse2), args.steps, args.warmup)
+        # Graph-replayed: a lone combine launch is shorter than its host-side call.
+        combine_ms = timed_graph(lambda: ops.combine(part_o, part_lse, out=out2, lse=lse2), max(20, args.steps // 4))
     kernel_ms = ms - combine_ms
 
     # No-rotation diagnostic: the same kernel with K rotation compiled out, over the unrotated store.
@@ -274,6 +455,9 @@ def main() -> int:
             "traffic": recorded_traffic("decode_kernel_rag_decode"),
         }
         del kmd, dd
+
+    if not args.no_other:
+        result["other_configs"] = other_configs(dev, args.steps, args.warmup, log)
 
     if args.copy_probe_mib > 0:
         n = args.copy_probe_mib * (1 << 20) // 4
