@@ -41,13 +41,23 @@ int prefill_q_tiles(const lazy_attn_params_t* p, int32_t max_q_len) {
   return (int)ceil_div((int64_t)max_q_len * g, (int64_t)lazy::kPrefillRowsPerBlock * prefill_row_blocks(p, max_q_len));
 }
 
-int prefill_splits(const lazy_attn_params_t* p, int32_t batch, int32_t max_q_len, int32_t max_kv_len) {
+// KV splits per request.  Workgroups are (query tile, KV head, request, split); those of a query tile past the end
+// of a shorter request exit at once, so the busy ones number about Hkv * ceil(total_q G / rows per tile) per split.
+// Equal requests: one round of workgroups over the chip.  Ragged query lengths (mean below 3/4 of the maximum)
+// usually come with ragged key lengths, and one round then leaves CUs idle behind the longest requests: aim for
+// about three rounds so that the dispatcher can even out the load.
+int prefill_splits(const lazy_attn_params_t* p, int32_t batch, int32_t total_q, int32_t max_q_len,
+                   int32_t max_kv_len) {
   if (p->num_splits > 0) return p->num_splits;
-  const int64_t base = (int64_t)prefill_q_tiles(p, max_q_len) * p->num_kv_heads * batch;
+  const int64_t g = p->num_q_heads / p->num_kv_heads;
+  const int64_t rows_per_tile = (int64_t)lazy::kPrefillRowsPerBlock * prefill_row_blocks(p, max_q_len);
+  const int64_t busy = (int64_t)p->num_kv_heads * ceil_div((int64_t)total_q * g, rows_per_tile);
   const int64_t tiles = ceil_div(max_kv_len, lazy::kPrefillTileKeys);
   // 256-row workgroups occupy a whole CU (LDS), 128-row ones leave room for two per CU.
-  const int64_t target = prefill_row_blocks(p, max_q_len) == 2 ? kNumCUs : 2 * kNumCUs;
-  int64_t s = base > 0 ? ceil_div(target, base) : 1;
+  const int64_t slots = prefill_row_blocks(p, max_q_len) == 2 ? kNumCUs : 2 * kNumCUs;
+  const bool ragged = 4 * (int64_t)total_q < 3 * (int64_t)batch * max_q_len;
+  const int64_t target = ragged ? 3 * slots : slots;
+  int64_t s = busy > 0 ? ceil_div(target, busy) : 1;
   const int64_t cap = tiles / 4 > 1 ? tiles / 4 : 1;  // keep at least ~4 key tiles per split
   if (s > cap) s = cap;
   if (s > 64) s = 64;
@@ -90,7 +100,7 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
   if (batch == 0 || total_q == 0) return LAZY_OK;
   if (max_q_len == 0) return LAZY_EINVAL;
   if (!q || !q_start || !q_pos0 || !k_pool || !v_pool || !chunks || !chunk_start || !out) return LAZY_EINVAL;
-  const int splits = prefill_splits(p, batch, max_q_len, max_kv_len);
+  const int splits = prefill_splits(p, batch, total_q, max_q_len, max_kv_len);
   const int q_tiles = prefill_q_tiles(p, max_q_len);
   if ((int64_t)batch * splits > 65535 || p->num_kv_heads > 65535) return LAZY_EUNSUPPORTED;
   const int64_t rows = (int64_t)total_q * p->num_q_heads;
@@ -177,7 +187,7 @@ extern "C" {
 size_t lazy_attn_prefill_workspace_size(const lazy_attn_params_t* params, int32_t batch, int32_t total_q,
                                         int32_t max_q_len, int32_t max_kv_len) {
   if (check_params(params) != LAZY_OK || batch <= 0 || total_q <= 0 || max_q_len <= 0 || max_kv_len < 0) return 0;
-  const int splits = prefill_splits(params, batch, max_q_len, max_kv_len);
+  const int splits = prefill_splits(params, batch, total_q, max_q_len, max_kv_len);
   return split_workspace(splits, (int64_t)total_q * params->num_q_heads, params->head_dim);
 }
 

@@ -69,6 +69,17 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // the chunk-table walk that depends on them runs as divergent vector code, its record loads become vector loads,
 // and their waits drain the vector-memory queue that holds the next tile's prefetched K / V.
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
 // Reductions over lane pairs (l, l ^ 32) with v_permlane32_swap (one VALU op, no LDS round trip).  Swapping a
 // register with itself yields x[l % 32] in one result and x[l % 32 + 32] in the other, in every lane, so both
 // lanes of a pair combine the same two values in the same order.
@@ -153,27 +164,45 @@ template <int TK>
 struct TileIter {
   cptr<lazy_chunk_t> recs;
   int i, end, j0, left;
-  Rec cur;
+  Rec cur, nxt;  // records i and i + 1 (nxt only while i + 1 < end): the next record is always loaded ahead
 
+  // The tile counts are taken one record per lane, 64 records at a time, with a wave-wide prefix sum, so that a long
+  // chunk table costs a few parallel loads rather than a chain of dependent ones.  Must be called by whole waves
+  // with wave-uniform arguments; every member ends up wave-uniform.
   __device__ void init(const lazy_chunk_t* table, int c0, int c1, int split, int splits) {
-    const cptr<lazy_chunk_t> chunks = as_const(table);
-    recs = chunks;
+    recs = as_const(table);
     end = c1;
-    int ntiles = 0;
-    for (int k = c0; k < c1; ++k) ntiles += (chunks[k].len + TK - 1) / TK;
+    const int lane = threadIdx.x & 63;
+    int ntiles = 0, nt0 = 0;
+    for (int k0 = c0; k0 < c1; k0 += 64) {
+      const int k = k0 + lane;
+      const int nt = k < c1 ? (table[k].len + TK - 1) / TK : 0;
+      if (k0 == c0) nt0 = nt;
+      ntiles += __builtin_amdgcn_readlane(wave_incl_scan(nt), 63);
+    }
     const int lo = (int)((int64_t)ntiles * split / splits);
     const int hi = (int)((int64_t)ntiles * (split + 1) / splits);
     left = hi - lo;
+    i = c1;
+    j0 = 0;
+    if (left <= 0) return;
+    // The record holding tile lo: the first whose inclusive tile count exceeds lo.
     int acc = 0;
-    i = c0;
-    while (i < c1) {
-      const int nt = (chunks[i].len + TK - 1) / TK;
-      if (acc + nt > lo) break;
-      acc += nt;
-      ++i;
+    for (int k0 = c0; k0 < c1; k0 += 64) {
+      const int k = k0 + lane;
+      const int nt = k0 == c0 ? nt0 : (k < c1 ? (table[k].len + TK - 1) / TK : 0);
+      const int incl = acc + wave_incl_scan(nt);
+      const uint64_t hit = __ballot(k < c1 && incl > lo);
+      if (hit) {
+        const int f = __builtin_ctzll(hit);
+        i = k0 + f;
+        j0 = (lo - __builtin_amdgcn_readlane(incl - nt, f)) * TK;
+        break;
+      }
+      acc = __builtin_amdgcn_readlane(incl, 63);
     }
-    j0 = (lo - acc) * TK;
-    if (left > 0) cur = load_rec(chunks + i);
+    cur = load_rec(recs + i);
+    if (i + 1 < end) nxt = load_rec(recs + i + 1);
   }
   __device__ void step() {
     --left;
@@ -182,7 +211,8 @@ struct TileIter {
     while (left > 0 && j0 >= cur.len) {
       ++i;
       j0 = 0;
-      cur = load_rec(recs + i);
+      cur = nxt;
+      if (i + 1 < end) nxt = load_rec(recs + i + 1);
     }
   }
   // Move to the next tile that some query of the workgroup can see (the current one included).
@@ -989,33 +1019,65 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 }
 
 // ---------------------------------------------------------------------------------------------------------------
-// Split-KV combine: out = sum_s e^{m_s - M} acc_s / sum_s e^{m_s - M} l_s.  D/4 threads per row, 4 dims each.
+// Split-KV merge: per row, the splits' normalised outputs weighted by exp(lse_s - max lse), divided by the sum of
+// the weights.  A row is served by kCombineGroups x D / 8 lanes of one wave: lane (g, d8) loads 8 dims (16 bytes)
+// of the splits g, g + kCombineGroups, ...; the groups' partial sums are then added across lanes.  Every thread
+// first reads all of the row's log-sum-exps (independent loads, one round trip), so a merge over many splits costs
+// two memory round trips rather than one per split.
 // ---------------------------------------------------------------------------------------------------------------
-// Split-KV merge: per row, the splits' normalised outputs weighted by exp(lse_s - max lse).  One row per D / 8
-// threads, 16-byte loads of bf16 partial rows.
+constexpr int kCombineGroups = 4;
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __restrict__ part_o,
                                                            const float* __restrict__ part_lse, int splits, int rows,
                                                            uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int TPR = D / 8;
-  const int row = blockIdx.x * (kThreads / TPR) + threadIdx.x / TPR;
+  constexpr int LPR = TPR * kCombineGroups;  // lanes per row: 64 (D = 128) or 32 (D = 64)
+  static_assert(LPR <= 64 && 64 % LPR == 0, "a row's lanes lie in one wave");
+  const int row = blockIdx.x * (kThreads / LPR) + threadIdx.x / LPR;
   const int d8 = threadIdx.x % TPR;
-  if (row >= rows) return;
+  const int grp = (threadIdx.x / TPR) % kCombineGroups;
+  // Rows past the end take part in the shuffles with no memory access (the whole wave stays converged).
+  const bool live = row < rows;
   float mmax = -INFINITY;
-  for (int s = 0; s < splits; ++s) mmax = fmaxf(mmax, part_lse[(int64_t)s * rows + row]);
-  float den = 0.f, sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  if (mmax != -INFINITY) {
-    for (int s = 0; s < splits; ++s) {
-      const int64_t w = (int64_t)s * rows + row;
-      const float ls = part_lse[w];
-      if (ls == -INFINITY) continue;
-      const float sc = expf(ls - mmax);
-      den += sc;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(part_o + w * D + 8 * d8);
+  if (live) {
+    for (int s0 = 0; s0 < splits; s0 += 8) {
+      float l[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sum[e] = fmaf((e & 1) ? bf_hi(v[e >> 1]) : bf_lo(v[e >> 1]), sc, sum[e]);
+      for (int e = 0; e < 8; ++e) l[e] = s0 + e < splits ? part_lse[(int64_t)(s0 + e) * rows + row] : -INFINITY;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) mmax = fmaxf(mmax, l[e]);
     }
   }
+  float den = 0.f, sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (live && mmax != -INFINITY) {
+    for (int s0 = grp; s0 < splits; s0 += 2 * kCombineGroups) {
+      float ls[2];
+      u32x4 v[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int sp = s0 + e * kCombineGroups;
+        const int64_t w = (int64_t)(sp < splits ? sp : s0) * rows + row;
+        ls[e] = sp < splits ? part_lse[w] : -INFINITY;
+        v[e] = *reinterpret_cast<const u32x4*>(part_o + w * D + 8 * d8);
+      }
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        if (ls[e] == -INFINITY) continue;  // an empty split contributes nothing, whatever its output holds
+        const float sc = expf(ls[e] - mmax);
+        den += sc;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) sum[k] = fmaf((k & 1) ? bf_hi(v[e][k >> 1]) : bf_lo(v[e][k >> 1]), sc, sum[k]);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = TPR; off < LPR; off *= 2) {
+    den += __shfl_xor(den, off);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) sum[k] += __shfl_xor(sum[k], off);
+  }
+  if (!live || grp != 0) return;
   const float inv = den > 0.f ? 1.f / den : 0.f;
   *reinterpret_cast<u32x4*>(out + (int64_t)row * D + 8 * d8) =
       u32x4{pack2(sum[0] * inv, sum[1] * inv), pack2(sum[2] * inv, sum[3] * inv), pack2(sum[4] * inv, sum[5] * inv),
@@ -1126,7 +1188,7 @@ hipError_t decode_d(const AttnArgs& a, hipStream_t st) {
 hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int splits, int rows, int head_dim,
                           uint16_t* out, float* lse, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  const int per_block = kThreads / (head_dim / 8);
+  const int per_block = kThreads / (head_dim / 8 * kCombineGroups);
   const dim3 grid((rows + per_block - 1) / per_block);
   if (head_dim == 128)
     hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, out, lse);

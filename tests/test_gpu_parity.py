@@ -185,9 +185,9 @@ def test_materialized_keys_match_oracle():
             base += 2 * n * 128
 
 
-def test_combine_entry_point_matches_oracle_merge():
-    rng = np.random.default_rng(5)
-    s, rows, d = 5, 37, 128
+@pytest.mark.parametrize("s,rows,d", [(5, 37, 128), (2, 300, 64), (13, 70, 128), (64, 9, 64)])
+def test_combine_entry_point_matches_oracle_merge(s, rows, d):
+    rng = np.random.default_rng(5 + s)
     m = rng.normal(0, 3, size=(s, rows))
     m[1, :4] = -np.inf  # empty splits
     m[:, 7] = -np.inf   # a row with no key at all
