@@ -173,12 +173,21 @@ struct TileIter {
     recs = as_const(table);
     end = c1;
     const int lane = threadIdx.x & 63;
-    int ntiles = 0, nt0 = 0;
-    for (int k0 = c0; k0 < c1; k0 += 64) {
-      const int k = k0 + lane;
-      const int nt = k < c1 ? (table[k].len + TK - 1) / TK : 0;
-      if (k0 == c0) nt0 = nt;
-      ntiles += __builtin_amdgcn_readlane(wave_incl_scan(nt), 63);
+    // Pass 1: the request's tile count.  Four blocks of 64 records are loaded at once; the first four stay in
+    // registers for pass 2.
+    int ntiles = 0, ntb[4];
+    for (int k0 = c0; k0 < c1; k0 += 256) {
+      int nt[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int k = k0 + 64 * u + lane;
+        nt[u] = k < c1 ? (table[k].len + TK - 1) / TK : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (k0 == c0) ntb[u] = nt[u];
+        ntiles += __builtin_amdgcn_readlane(wave_incl_scan(nt[u]), 63);
+      }
     }
     const int lo = (int)((int64_t)ntiles * split / splits);
     const int hi = (int)((int64_t)ntiles * (split + 1) / splits);
@@ -186,11 +195,13 @@ struct TileIter {
     i = c1;
     j0 = 0;
     if (left <= 0) return;
-    // The record holding tile lo: the first whose inclusive tile count exceeds lo.
+    // Pass 2: the record holding tile lo, the first whose inclusive tile count exceeds lo.
     int acc = 0;
     for (int k0 = c0; k0 < c1; k0 += 64) {
       const int k = k0 + lane;
-      const int nt = k0 == c0 ? nt0 : (k < c1 ? (table[k].len + TK - 1) / TK : 0);
+      const int b = (k0 - c0) >> 6;
+      const int nt = b < 4 ? (b == 0 ? ntb[0] : b == 1 ? ntb[1] : b == 2 ? ntb[2] : ntb[3])
+                           : (k < c1 ? (table[k].len + TK - 1) / TK : 0);
       const int incl = acc + wave_incl_scan(nt);
       const uint64_t hit = __ballot(k < c1 && incl > lo);
       if (hit) {
@@ -260,16 +271,15 @@ __device__ __forceinline__ u32x2 tr_read(const uint16_t* p) {
 template <int D>
 __device__ __forceinline__ int cs_idx(int t) { return 2 * t + 8 * (t / (D / 8)); }
 
-// Four query pairs (t0..t0+3 with their partners t0+D/2..) of one query row, rotated at position p, as one 8-element
+// Four query pairs (t0..t0+3 with their partners t0+D/2..) of one query row (raw bf16: lo = elements t0..t0+3,
+// hi = t0+D/2..t0+D/2+3), rotated at position p, as one 8-element
 // MFMA fragment in virtual order [low t0..t0+3, high t0..t0+3].  The angles follow the decomposition used for the
 // keys: cos/sin(p theta_t) from the query block
 // base (qb: position 32 (p / 32)) and the per-row delta table (qd: row p % 32), one angle addition per pair.
 template <int D>
-__device__ __forceinline__ bf16x8 q_fragment_tab(const uint16_t* qrow, int t0, const float* qb, const float* qd,
+__device__ __forceinline__ bf16x8 q_fragment_tab(u32x2 lo, u32x2 hi, int t0, const float* qb, const float* qd,
                                                  bool valid) {
   if (!valid) return as_bf16x8(u32x4{0, 0, 0, 0});
-  const u32x2 lo = *reinterpret_cast<const u32x2*>(qrow + t0);
-  const u32x2 hi = *reinterpret_cast<const u32x2*>(qrow + D / 2 + t0);
   const f32x4 b01 = reinterpret_cast<const f32x4*>(qb + cs_idx<D>(t0))[0];
   const f32x4 b23 = reinterpret_cast<const f32x4*>(qb + cs_idx<D>(t0))[1];
   const f32x4 d01 = reinterpret_cast<const f32x4*>(qd + cs_idx<D>(t0))[0];
@@ -331,7 +341,8 @@ __device__ __forceinline__ int kblk_t(int b) {
 }
 
 // Cooperative loader of one 64-key tile for the prefill kernel with NT threads: TPR = NT / 64 threads per key row,
-// each rotating PP = D / (2 TPR) pairs; V copied row-major in 16-byte chunks (VC per thread).
+// each rotating PP = D / (2 TPR) pairs of its row; V copied row-major in 16-byte chunks (VC per thread, of the same
+// row, so that a thread's share of K and V is one key row: threads 0..NT/2-1 hold rows 0..31).
 // The per-row cos/sin constants are written to a private LDS slice once per workgroup and read per tile.
 template <int D, bool ROT, int NT, bool CSD_REGS = false>
 struct PLoader {
@@ -341,6 +352,7 @@ struct PLoader {
   static constexpr int NV = PP / 8;
   static constexpr int VC = kSub * (D / 8) / NT;
   static_assert(PP % 8 == 0, "each loader thread rotates whole groups of 8 pairs");
+  static_assert(VC * TPR == D / 8, "a row's V chunks are shared by its TPR threads");
   u32x4 klo[NV], khi[NV];
   u32x4 vr[VC];
   float2 cdr[CSD_REGS && ROT ? PP : 1];
@@ -371,10 +383,8 @@ struct PLoader {
         khi[v] = reinterpret_cast<const u32x4*>(src + D / 2)[v];
       }
 #pragma unroll
-      for (int i = 0; i < VC; ++i) {
-        const int c = tid + NT * i;
-        vr[i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)(c / (D / 8)) * D + 8 * (c % (D / 8)));
-      }
+      for (int i = 0; i < VC; ++i)
+        vr[i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)row * D + 8 * (part + TPR * i));
       return;
     }
     const bool ok = row < nvalid;
@@ -388,11 +398,8 @@ struct PLoader {
     }
 #pragma unroll
     for (int i = 0; i < VC; ++i) {
-      const int c = tid + NT * i;
-      const int rr = c / (D / 8);
-      const bool vok = rr < nvalid;
-      const u32x4 x = *reinterpret_cast<const u32x4*>(vbase + (size_t)(vok ? rr : 0) * D + 8 * (c % (D / 8)));
-      vr[i] = vok ? x : zero;
+      const u32x4 x = *reinterpret_cast<const u32x4*>(vbase + (size_t)(ok ? row : 0) * D + 8 * (part + TPR * i));
+      vr[i] = ok ? x : zero;
     }
   }
 
@@ -425,10 +432,7 @@ struct PLoader {
       *reinterpret_cast<u32x4*>(krow + 8 * kblk_t<TPR>(t0 / 4 + 1)) = w1;
     }
 #pragma unroll
-    for (int i = 0; i < VC; ++i) {
-      const int c = tid + NT * i;
-      *reinterpret_cast<u32x4*>(vtbuf + (c / (D / 8)) * S::VLD + 8 * (c % (D / 8))) = vr[i];
-    }
+    for (int i = 0; i < VC; ++i) *reinterpret_cast<u32x4*>(vtbuf + row * S::VLD + 8 * (part + TPR * i)) = vr[i];
   }
 };
 
@@ -439,6 +443,137 @@ __device__ __forceinline__ void prefill_base(float* csb2, const double* freq, in
     const int h = tid / (D / 2), t = tid % (D / 2);
     *reinterpret_cast<float2*>(csb2 + h * TileLayout<D>::CSW + cs_idx<D>(t)) = rope_cs(b0 + kAngleRows * h, freq[t]);
   }
+}
+
+// V^T fragments of 16-key step s2 for the four 32-dimension blocks (two transposing reads each).
+template <int D>
+__device__ __forceinline__ void v_fragments(const uint16_t* vlane, int s2, u32x4 (&vv)[D / 32]) {
+  using S = TileLayout<D>;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) {
+    const u32x2 lo = tr_read(vlane + (16 * s2) * S::VLD + 32 * db);
+    const u32x2 hi = tr_read(vlane + (16 * s2 + 8) * S::VLD + 32 * db);
+    vv[db] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+  }
+}
+
+// One 64-key tile for one wave's RB blocks of 32 query rows: S^T = K Q^T on the matrix cores, the key mask (tile
+// tail and position-based causal rule), the online-softmax update with lazy rescaling, and O^T += V^T P^T.
+// kb / vt: the tile's rotated K and row-major V in LDS; b0: position of the tile's first key; nvalid: keys in the
+// tile; qmin: smallest query position of the workgroup (tiles entirely at or before it need no causal mask).
+template <int D, int NT, int RB>
+__device__ __forceinline__ void attend_tile(const uint16_t* kb, const uint16_t* vt, int lane,
+                                            const bf16x8 (&qf)[RB][D / 16], f32x16 (&o)[RB][D / 32],
+                                            float (&m2)[RB], float (&lsum)[RB], const int (&qpos)[RB], int b0,
+                                            int nvalid, int qmin, int causal, float c) {
+  using S = TileLayout<D>;
+  const int h2 = lane >> 5;
+  // Transposing-read address of this lane in the V tile: row 4*(g/2) + i/4 (+ 16 per key step, + 8 for the
+  // second half of the fragment), column 16*(g%2) + 4*(i%4) (+ 32 per dimension block); g = lane/16, i = lane%16.
+  const uint16_t* vlane = vt + (4 * ((lane >> 4) >> 1) + ((lane & 15) >> 2)) * S::VLD +
+                          16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  // S^T = K Q^T: two 32-key blocks per row block; each K fragment feeds RB MFMAs.  Fragments are read one
+  // k-step ahead and the scheduler is fenced per k-step, which bounds the registers held by in-flight reads.
+  f32x16 sa[RB][2];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) sa[rb][0] = sa[rb][1] = f32x16{};
+  // Waves raise their issue priority while they feed the matrix cores, so that the MFMA blocks of one wave run
+  // ahead and the other wave's softmax / rotation VALU work fills the gaps.
+  __builtin_amdgcn_s_setprio(1);
+  {
+    const uint16_t* kl = kb + (lane & 31) * S::KLD;
+    u32x4 kv[2][2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+      kv[0][blk] = *reinterpret_cast<const u32x4*>(kl + 32 * blk * S::KLD + 8 * kblk_t<NT / kSub>(h2));
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) {
+      if (s + 1 < D / 16) {
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+          kv[(s + 1) & 1][blk] = *reinterpret_cast<const u32x4*>(kl + 32 * blk * S::KLD +
+                                                                 8 * kblk_t<NT / kSub>(2 * (s + 1) + h2));
+      }
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          sa[rb][blk] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv[s & 1][blk]), qf[rb][s], sa[rb][blk], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  __builtin_amdgcn_s_setprio(0);
+  if (nvalid < kSub || (causal && b0 + kSub - 1 > qmin)) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int kk = 32 * blk + 8 * (i >> 2) + 4 * h2 + (i & 3);
+          const bool ok = kk < nvalid && (!causal || b0 + kk <= qpos[rb]);
+          if (!ok) sa[rb][blk][i] = -INFINITY;
+        }
+  }
+  uint32_t pk[RB][16];  // bf16 pairs of P: block blk, keys 8 (i / 4) + 4 h2 + i % 4 for i = 2 j, 2 j + 1
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sa[rb][blk][i]);
+    mx = xor32_max(mx);
+    // Lazy rescale: the reference max only moves when this tile's max exceeds it by more than kRescaleSlack.
+    const float mt = mx * c;
+    if (__any(mt > m2[rb] + kRescaleSlack)) {
+      const float mnew = fmaxf(m2[rb], mt);
+      const float alpha = m2[rb] == -INFINITY ? 0.f : fast_exp2(m2[rb] - mnew);
+      lsum[rb] *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) o[rb][db] *= alpha;
+      m2[rb] = mnew;
+    }
+    const float muse = m2[rb] == -INFINITY ? 0.f : m2[rb];
+    float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t pp = pack2(fast_exp2(fmaf(sa[rb][blk][2 * j], c, -muse)),
+                                  fast_exp2(fmaf(sa[rb][blk][2 * j + 1], c, -muse)));
+        pk[rb][8 * blk + j] = pp;
+        if (j & 1)
+          ps1 = add_pair(pp, ps1);
+        else
+          ps0 = add_pair(pp, ps0);
+      }
+    lsum[rb] += ps0 + ps1;
+  }
+
+  // O^T += V^T P^T: four 16-key steps; each V fragment feeds RB MFMAs (same bounded read-ahead).
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int s2 = 0; s2 < 4; ++s2) {
+    bf16x8 pb[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int j0 = 8 * (s2 >> 1) + 4 * (s2 & 1);
+      pb[rb] = as_bf16x8(u32x4{pk[rb][j0], pk[rb][j0 + 1], pk[rb][j0 + 2], pk[rb][j0 + 3]});
+    }
+    u32x4 vv[D / 32];
+    v_fragments<D>(vlane, s2, vv);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        o[rb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv[db]), pb[rb], o[rb][db], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  __builtin_amdgcn_s_setprio(0);
 }
 
 template <int D, bool ROT, int NW, int NBUF, int RB>
@@ -462,9 +597,6 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   if (row0 >= nrows) return;
   const int qp0 = as_const(a.q_pos0)[r];
 
-  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
-  __syncthreads();
-
   const int h2 = lane >> 5;
   bool rvalid[RB];
   int tok[RB], head[RB], qpos[RB];
@@ -478,6 +610,34 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   }
   const int last = min(row0 + BM, nrows) - 1;
   const int qmin = uniform(qp0 + row0 / G), qmax = uniform(qp0 + last / G);
+
+  // Raw Q first, then the chunk-table walk and the first tile's K / V: the angle tables and the Q rotation below
+  // are computed while those loads are in flight (Q, issued first, is waited for without waiting for the tile).
+  u32x2 qraw[RB][D / 16][2];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const uint16_t* qrow = a.q + ((int64_t)(qs + tok[rb]) * a.hq + head[rb]) * D;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) {
+      const int t0 = 8 * s + 4 * h2;
+      qraw[rb][s][0] = qraw[rb][s][1] = u32x2{0, 0};
+      if (rvalid[rb]) {
+        qraw[rb][s][0] = *reinterpret_cast<const u32x2*>(qrow + t0);
+        qraw[rb][s][1] = *reinterpret_cast<const u32x2*>(qrow + D / 2 + t0);
+      }
+    }
+  }
+  PLoader<D, ROT, NT, RB == 2> ld;
+  ld.init(tid);
+  TileIter<kSub> it;
+  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
+  bool have = it.seek(a.causal, qmax);
+  if (have)
+    ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+             min(kSub, it.cur.len - it.j0));
+
+  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
+  __syncthreads();
 
   // Angle tables: per-row deltas cos/sin(delta theta_t), delta < 32 (queries and keys), and the query block bases
   // cos/sin(32 a theta_t), a = qmin / 32 .. qmax / 32.
@@ -493,11 +653,11 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   bf16x8 qf[RB][D / 16];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const uint16_t* qrow = a.q + ((int64_t)(qs + tok[rb]) * a.hq + head[rb]) * D;
     const float* qbr = sm.qb[qpos[rb] / kAngleRows - qa0];
     const float* qdr = sm.csd + (qpos[rb] & (kAngleRows - 1)) * S::CSD_LD;
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s) qf[rb][s] = q_fragment_tab<D>(qrow, 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
+    for (int s = 0; s < D / 16; ++s)
+      qf[rb][s] = q_fragment_tab<D>(qraw[rb][s][0], qraw[rb][s][1], 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
   }
 
   f32x16 o[RB][D / 32];
@@ -511,28 +671,19 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   }
   const float c = a.scale_log2;
 
-  PLoader<D, ROT, NT, RB == 2> ld;
-  ld.init(tid);
   ld.load_constants(sm.csd);
-  TileIter<kSub> it;
-  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
-  bool have = it.seek(a.causal, qmax);
 
   // Tile "ahead" state for NBUF == 2: position of the tile after the current one.
   TileIter<kSub> ahead = it;
   bool have_ahead = false;
-  if (have) {
-    ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
-             min(kSub, it.cur.len - it.j0));
-    if (NBUF == 2) {
-      if (ROT) prefill_base<D>(sm.csb[0][0], sm.freq, tid, it.cur.pos + it.j0);
-      ahead.step();
-      have_ahead = ahead.seek(a.causal, qmax);
-      if (ROT && have_ahead) prefill_base<D>(sm.csb[1][0], sm.freq, tid, ahead.cur.pos + ahead.j0);
-      __syncthreads();
-      ld.store(sm.k[0], sm.v[0], sm.csb[0][0], sm.csd);
-      __syncthreads();
-    }
+  if (have && NBUF == 2) {
+    if (ROT) prefill_base<D>(sm.csb[0][0], sm.freq, tid, it.cur.pos + it.j0);
+    ahead.step();
+    have_ahead = ahead.seek(a.causal, qmax);
+    if (ROT && have_ahead) prefill_base<D>(sm.csb[1][0], sm.freq, tid, ahead.cur.pos + ahead.j0);
+    __syncthreads();
+    ld.store(sm.k[0], sm.v[0], sm.csb[0][0], sm.csd);
+    __syncthreads();
   }
   int parity = 0;
   while (have) {
@@ -561,118 +712,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
         have_ahead = ahead.seek(a.causal, qmax);
       }
     }
-    const uint16_t* kb = sm.k[cur_buf];
-    // Transposing-read address of this lane in the V tile: row 4*(g/2) + i/4 (+ 16 per key step, + 8 for the
-    // second half of the fragment), column 16*(g%2) + 4*(i%4) (+ 32 per dimension block); g = lane/16, i = lane%16.
-    const uint16_t* vlane = sm.v[cur_buf] + (4 * ((lane >> 4) >> 1) + ((lane & 15) >> 2)) * S::VLD +
-                            16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-
-    // S^T = K Q^T: two 32-key blocks per row block; each K fragment feeds RB MFMAs.  Fragments are read one
-    // k-step ahead and the scheduler is fenced per k-step, which bounds the registers held by in-flight reads.
-    f32x16 sa[RB][2];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) sa[rb][0] = sa[rb][1] = f32x16{};
-    // Waves raise their issue priority while they feed the matrix cores, so that the MFMA blocks of one wave run
-    // ahead and the other wave's softmax / rotation VALU work fills the gaps.
-    __builtin_amdgcn_s_setprio(1);
-    {
-      const uint16_t* kl = kb + (lane & 31) * S::KLD;
-      u32x4 kv[2][2];
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-        kv[0][blk] = *reinterpret_cast<const u32x4*>(kl + 32 * blk * S::KLD + 8 * kblk_t<NT / kSub>(h2));
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
-        if (s + 1 < D / 16) {
-#pragma unroll
-          for (int blk = 0; blk < 2; ++blk)
-            kv[(s + 1) & 1][blk] = *reinterpret_cast<const u32x4*>(kl + 32 * blk * S::KLD +
-                                                                   8 * kblk_t<NT / kSub>(2 * (s + 1) + h2));
-        }
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-            sa[rb][blk] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv[s & 1][blk]), qf[rb][s], sa[rb][blk], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-    __builtin_amdgcn_s_setprio(0);
-    if (nvalid < kSub || (a.causal && b0 + kSub - 1 > qmin)) {
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int kk = 32 * blk + 8 * (i >> 2) + 4 * h2 + (i & 3);
-            const bool ok = kk < nvalid && (!a.causal || b0 + kk <= qpos[rb]);
-            if (!ok) sa[rb][blk][i] = -INFINITY;
-          }
-    }
-    uint32_t pk[RB][16];  // bf16 pairs of P: block blk, keys 8 (i / 4) + 4 h2 + i % 4 for i = 2 j, 2 j + 1
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sa[rb][blk][i]);
-      mx = xor32_max(mx);
-      // Lazy rescale: the reference max only moves when this tile's max exceeds it by more than kRescaleSlack.
-      const float mt = mx * c;
-      if (__any(mt > m2[rb] + kRescaleSlack)) {
-        const float mnew = fmaxf(m2[rb], mt);
-        const float alpha = m2[rb] == -INFINITY ? 0.f : fast_exp2(m2[rb] - mnew);
-        lsum[rb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) o[rb][db] *= alpha;
-        m2[rb] = mnew;
-      }
-      const float muse = m2[rb] == -INFINITY ? 0.f : m2[rb];
-      float ps0 = 0.f, ps1 = 0.f;
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const uint32_t pp = pack2(fast_exp2(fmaf(sa[rb][blk][2 * j], c, -muse)),
-                                    fast_exp2(fmaf(sa[rb][blk][2 * j + 1], c, -muse)));
-          pk[rb][8 * blk + j] = pp;
-          if (j & 1)
-            ps1 = add_pair(pp, ps1);
-          else
-            ps0 = add_pair(pp, ps0);
-        }
-      lsum[rb] += ps0 + ps1;
-    }
-
-    // O^T += V^T P^T: four 16-key steps; each V fragment feeds RB MFMAs (same bounded read-ahead).
-    __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int s2 = 0; s2 < 4; ++s2) {
-      bf16x8 pb[RB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const int j0 = 8 * (s2 >> 1) + 4 * (s2 & 1);
-        pb[rb] = as_bf16x8(u32x4{pk[rb][j0], pk[rb][j0 + 1], pk[rb][j0 + 2], pk[rb][j0 + 3]});
-      }
-      u32x4 vv[D / 32];
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        const u32x2 lo = tr_read(vlane + (16 * s2) * S::VLD + 32 * db);
-        const u32x2 hi = tr_read(vlane + (16 * s2 + 8) * S::VLD + 32 * db);
-        vv[db] = u32x4{lo[0], lo[1], hi[0], hi[1]};
-      }
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          o[rb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv[db]), pb[rb], o[rb][db], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-
-    __builtin_amdgcn_s_setprio(0);
+    attend_tile<D, NT, RB>(sm.k[cur_buf], sm.v[cur_buf], lane, qf, o, m2, lsum, qpos, b0, nvalid, qmin, a.causal, c);
     if (NBUF == 2) {
       // Base angles two tiles ahead go to the table slot this tile used; the next tile goes to the other buffer.
       if (ROT && have_ahead) prefill_base<D>(sm.csb[parity][0], sm.freq, tid, ahead.cur.pos + ahead.j0);
@@ -804,6 +844,33 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int col = lane & 15, kq = lane >> 4;
   const int qpos = as_const(a.q_pos0)[r];
 
+  const bool hvalid = col < hcount;
+  const int head = g * G + kDecodeHeadsPerGroup * hg + (hvalid ? col : 0);
+  // Raw Q first, then the chunk-table walk and the first tile's K / V: the tables and the Q rotation below are
+  // computed while those loads are in flight (Q, issued first, is waited for without waiting for the tile).
+  u32x4 qraw[SP][2];
+  {
+    const uint16_t* qrow = a.q + ((int64_t)r * a.hq + head) * D;
+#pragma unroll
+    for (int s = 0; s < SP; ++s) {
+      const int t0 = 32 * s + 8 * kq;
+      qraw[s][0] = qraw[s][1] = u32x4{0, 0, 0, 0};
+      if (hvalid) {
+        qraw[s][0] = *reinterpret_cast<const u32x4*>(qrow + t0);
+        qraw[s][1] = *reinterpret_cast<const u32x4*>(qrow + D / 2 + t0);
+      }
+    }
+  }
+  // This wave's tiles: every fourth tile of the split, starting at tile `wave`.
+  TileIter<kDecWaveKeys> it;
+  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
+  for (int k = 0; k < wave && it.left > 0; ++k) it.step();
+  bool have = it.seek(a.causal, qpos);
+  DecTile<D> cur, nxt;
+  if (have)
+    dec_fetch<D>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+                 min(kDecWaveKeys, it.cur.len - it.j0), lane);
+
   if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
   __syncthreads();
   if (ROT) {
@@ -812,33 +879,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       const int dr = e / (D / 2), t = e % (D / 2);
       *reinterpret_cast<float2*>(sm.csd + dr * S::CSD_LD + 2 * t) = rope_cs(dr, sm.freq[t]);
     }
+    if (have && lane < D / 2)
+      *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
   }
-
-  const bool hvalid = col < hcount;
-  const int head = g * G + kDecodeHeadsPerGroup * hg + (hvalid ? col : 0);
   // Q fragments in the decode head-dimension order, rotated at the query position.
   bf16x8 qf[D / 32];
-  {
-    const uint16_t* qrow = a.q + ((int64_t)r * a.hq + head) * D;
 #pragma unroll
-    for (int s = 0; s < SP; ++s) {
-      float y1[8], y2[8];
-      const int t0 = 32 * s + 8 * kq;
-      u32x4 lo = {0, 0, 0, 0}, hi = {0, 0, 0, 0};
-      if (hvalid) {
-        lo = *reinterpret_cast<const u32x4*>(qrow + t0);
-        hi = *reinterpret_cast<const u32x4*>(qrow + D / 2 + t0);
-      }
+  for (int s = 0; s < SP; ++s) {
+    float y1[8], y2[8];
+    const int t0 = 32 * s + 8 * kq;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x1 = (e & 1) ? bf_hi(lo[e >> 1]) : bf_lo(lo[e >> 1]);
-        const float x2 = (e & 1) ? bf_hi(hi[e >> 1]) : bf_lo(hi[e >> 1]);
-        rotate_q_pair(x1, x2, qpos, sm.freq[t0 + e], y1[e], y2[e]);
-      }
-      qf[2 * s] = as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])});
-      qf[2 * s + 1] =
-          as_bf16x8(u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])});
+    for (int e = 0; e < 8; ++e) {
+      const float x1 = (e & 1) ? bf_hi(qraw[s][0][e >> 1]) : bf_lo(qraw[s][0][e >> 1]);
+      const float x2 = (e & 1) ? bf_hi(qraw[s][1][e >> 1]) : bf_lo(qraw[s][1][e >> 1]);
+      rotate_q_pair(x1, x2, qpos, sm.freq[t0 + e], y1[e], y2[e]);
     }
+    qf[2 * s] = as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])});
+    qf[2 * s + 1] = as_bf16x8(u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])});
   }
   __syncthreads();  // per-row table complete
 
@@ -854,20 +911,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const uint16_t* vlane = vw + (16 * (kq >> 1) + 4 * (kq & 1) + ((lane & 15) >> 2)) * S::VLD + 4 * (lane & 3);
   const float* cd0 = sm.csd + kappa(0, col) * S::CSD_LD;
   const float* cd1 = sm.csd + kappa(1, col) * S::CSD_LD;
-
-  // This wave's tiles: every fourth tile of the split, starting at tile `wave`.
-  TileIter<kDecWaveKeys> it;
-  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
-  for (int k = 0; k < wave && it.left > 0; ++k) it.step();
-  bool have = it.seek(a.causal, qpos);
-  DecTile<D> cur, nxt;
   int buf = 0;
-  if (have) {
-    dec_fetch<D>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
-                 min(kDecWaveKeys, it.cur.len - it.j0), lane);
-    if (ROT && lane < D / 2)
-      *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
-  }
   while (have) {
     const int nvalid = min(kDecWaveKeys, it.cur.len - it.j0);
     const int b0 = it.cur.pos + it.j0;
