@@ -19,6 +19,12 @@ plain definition, written out without tiling, online softmax or any reordering:
 5. Full-row softmax with max subtraction; o = sum(w v) / sum(w); lse = m + ln(sum(w)).  A query that sees no key
    gets o = 0 and lse = -inf.
 
+Key stores come in two conventions (``key_positions``).  "nope": keys are stored without any rotation and key j of a
+record is encoded at pos_offset + j (step 2).  "local": the paper's own convention (Sec. 3.2 "Prefilling": each
+document's cache keeps local positions indexed from 0, and reuse at offset Delta applies one fixed rotation to the
+whole document): the stored key j is already encoded at position j, and re-encoding it at pos_offset + j is the
+single rotation R(pos_offset) of the stored vector (the relative-rotation Fact, R(a) R(b) = R(a + b)).
+
 Decode is the same computation with one query token per request.  ``merge_partials`` is the plain definition of
 combining softmax statistics computed over disjoint key sets.  Parity for all of this is pinned by the CPU tests
 (textbook RoPE attention at contiguous positions, the relative-rotation Fact of Sec. 3.2, the rotate-the-query
@@ -54,14 +60,16 @@ def rotate(x: np.ndarray, positions: np.ndarray, theta: np.ndarray) -> np.ndarra
     return np.concatenate([x1 * c - x2 * s, x1 * s + x2 * c], axis=-1)
 
 
-def request_kv(pool_k, pool_v, chunks, lo: int, hi: int, num_kv_heads: int, head_dim: int):
-    """Gather one request's position-free K, V (in chunk-table order) and the position of every key.
+def request_kv(pool_k, pool_v, chunks, lo: int, hi: int, num_kv_heads: int, head_dim: int,
+               with_offsets: bool = False):
+    """Gather one request's stored K, V (in chunk-table order) and the position of every key.
 
     Record i covers keys j < len at position pos_offset + j; head g of that key is stored at
     k_offset + (g * k_stride + j) * D (V likewise with v_offset / v_stride).
-    Returns K [Hkv, L, D], V [Hkv, L, D] (fp64) and positions [L] (int64).
+    Returns K [Hkv, L, D], V [Hkv, L, D] (fp64) and positions [L] (int64); with ``with_offsets`` also the
+    pos_offset of every key's record [L].
     """
-    ks, vs, ps = [], [], []
+    ks, vs, ps, os_ = [], [], [], []
     d = head_dim
     for i in range(lo, hi):
         rec = chunks[i]
@@ -78,10 +86,23 @@ def request_kv(pool_k, pool_v, chunks, lo: int, hi: int, num_kv_heads: int, head
         ks.append(k)
         vs.append(v)
         ps.append(int(rec["pos_offset"]) + np.arange(n, dtype=np.int64))
+        os_.append(np.full(n, int(rec["pos_offset"]), dtype=np.int64))
     if not ks:
         z = np.zeros((num_kv_heads, 0, d))
-        return z, z.copy(), np.zeros(0, dtype=np.int64)
-    return np.concatenate(ks, axis=1), np.concatenate(vs, axis=1), np.concatenate(ps)
+        e = np.zeros(0, dtype=np.int64)
+        return (z, z.copy(), e, e.copy()) if with_offsets else (z, z.copy(), e)
+    res = (np.concatenate(ks, axis=1), np.concatenate(vs, axis=1), np.concatenate(ps))
+    return res + (np.concatenate(os_),) if with_offsets else res
+
+
+def key_rotation_positions(kpos, offs, key_positions: str):
+    """Position by which each stored key is rotated: its full position for a NoPE store, its record's pos_offset
+    for a local-position store (the key is already encoded at its local index j)."""
+    if key_positions == "nope":
+        return kpos
+    if key_positions == "local":
+        return offs
+    raise ValueError(f"unknown key_positions {key_positions!r}")
 
 
 def attend(q_rot, k_rot, v, q_pos, k_pos, causal: bool, scale: float):
@@ -118,10 +139,11 @@ def attend(q_rot, k_rot, v, q_pos, k_pos, causal: bool, scale: float):
 
 def lazy_attention(q, q_start, q_pos0, pool_k, pool_v, chunks, chunk_start, num_q_heads: int, num_kv_heads: int,
                    head_dim: int, rope_base: float, causal: bool = True, softmax_scale: float | None = None,
-                   inv_freq=None, requests=None):
+                   inv_freq=None, requests=None, key_positions: str = "nope"):
     """Attention of every request's query tokens over its chunk table, keys re-encoded at their positions.
 
     q [total_q, Hq, D] (NoPE queries), q_start [B+1], q_pos0 [B]: token i of request r is at q_pos0[r] + i.
+    key_positions: "nope" or "local" store convention (module docstring).
     Returns out [total_q, Hq, D] and lse [total_q, Hq] in fp64.  ``requests`` restricts the work to a subset of
     request indices (other rows stay 0 / -inf).
     """
@@ -136,10 +158,10 @@ def lazy_attention(q, q_start, q_pos0, pool_k, pool_v, chunks, chunk_start, num_
         a, b = int(q_start[r]), int(q_start[r + 1])
         if b == a:
             continue
-        k, v, kpos = request_kv(pool_k, pool_v, chunks, int(chunk_start[r]), int(chunk_start[r + 1]),
-                                num_kv_heads, head_dim)
+        k, v, kpos, offs = request_kv(pool_k, pool_v, chunks, int(chunk_start[r]), int(chunk_start[r + 1]),
+                                      num_kv_heads, head_dim, with_offsets=True)
         qpos = int(q_pos0[r]) + np.arange(b - a, dtype=np.int64)
-        k_rot = rotate(k, kpos, theta)  # explicit re-encoded copy of K
+        k_rot = rotate(k, key_rotation_positions(kpos, offs, key_positions), theta)  # explicit re-encoded copy
         q_rot = rotate(np.swapaxes(np.asarray(q[a:b], dtype=np.float64), 0, 1), qpos, theta)  # [Hq, Lq, D]
         o, l = attend(np.swapaxes(q_rot, 0, 1), k_rot, v, qpos, kpos, causal, scale)
         out[a:b] = o
@@ -148,23 +170,24 @@ def lazy_attention(q, q_start, q_pos0, pool_k, pool_v, chunks, chunk_start, num_
 
 
 def lazy_decode(q, q_pos, pool_k, pool_v, chunks, chunk_start, num_q_heads, num_kv_heads, head_dim, rope_base,
-                causal=True, softmax_scale=None, inv_freq=None, requests=None):
+                causal=True, softmax_scale=None, inv_freq=None, requests=None, key_positions: str = "nope"):
     """One query token per request at q_pos[r] (decode, Sec. 3.2 "Decoding"): q [B, Hq, D]."""
     batch = len(q_pos)
     q_start = np.arange(batch + 1)
     return lazy_attention(q, q_start, q_pos, pool_k, pool_v, chunks, chunk_start, num_q_heads, num_kv_heads,
-                          head_dim, rope_base, causal, softmax_scale, inv_freq, requests)
+                          head_dim, rope_base, causal, softmax_scale, inv_freq, requests, key_positions)
 
 
-def materialize_k(pool_k, chunks, chunk_start, num_kv_heads: int, head_dim: int, rope_base: float, inv_freq=None):
+def materialize_k(pool_k, chunks, chunk_start, num_kv_heads: int, head_dim: int, rope_base: float, inv_freq=None,
+                  key_positions: str = "nope"):
     """Re-encoded key copy of every request (the materialise-then-attend baseline's first step): a list over
-    requests of K' [Hkv, L_r, D], keys in chunk-table order, each rotated at pos_offset + j."""
+    requests of K' [Hkv, L_r, D], keys in chunk-table order, each encoded at pos_offset + j."""
     theta = rope_frequencies(head_dim, rope_base, inv_freq)
     res = []
     for r in range(len(chunk_start) - 1):
-        k, _, kpos = request_kv(pool_k, pool_k, chunks, int(chunk_start[r]), int(chunk_start[r + 1]),
-                                num_kv_heads, head_dim)
-        res.append(rotate(k, kpos, theta))
+        k, _, kpos, offs = request_kv(pool_k, pool_k, chunks, int(chunk_start[r]), int(chunk_start[r + 1]),
+                                      num_kv_heads, head_dim, with_offsets=True)
+        res.append(rotate(k, key_rotation_positions(kpos, offs, key_positions), theta))
     return res
 
 

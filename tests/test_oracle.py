@@ -379,3 +379,89 @@ def test_brute_force_decode_with_capacity_slack():
     assert (w.chunks["k_stride"] > w.chunks["len"]).any()
     out, _ = run(w)
     np.testing.assert_allclose(out, brute_force(w), rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------------------------------------------
+# Local-position key stores (Sec. 3.2 "Prefilling": each document's cache is kept at local positions from 0 and
+# reused at offset Delta with one fixed rotation; "Decoding": the query is rotated by the relative offset instead).
+# ---------------------------------------------------------------------------------------------------------------
+def local_store_from_nope(w):
+    """A local-position copy of a NoPE pool, written independently of the oracle: capacity slot j of every physical
+    chunk's K is multiplied, as the complex vector x_t + i x_{t+D/2}, by exp(i j theta_t).  V is left alone."""
+    d = w.head_dim
+    half = d // 2
+    theta = np.array([w.rope_base ** (-2.0 * t / d) for t in range(half)])
+    pool = w.pool.astype(np.float64).copy()
+    done = set()
+    for rec in w.chunks:
+        ko, cap = int(rec["k_offset"]), int(rec["k_stride"])
+        if ko in done:
+            continue
+        done.add(ko)
+        for g in range(w.num_kv_heads):
+            for j in range(cap):
+                a = ko + (g * cap + j) * d
+                x = pool[a: a + d]
+                z = (x[:half] + 1j * x[half:]) * np.exp(1j * j * theta)
+                pool[a: a + d] = np.concatenate([z.real, z.imag])
+    return pool
+
+
+def test_local_store_bridge_identity_prefill():
+    """k_local = R(j) k_nope: a local-position store used with one rotation by pos_offset gives exactly the NoPE
+    store's attention (shared chunks at different offsets, a causal query chunk, GQA)."""
+    w = W.rag_prefill(seed=21, batch=3, hq=4, hkv=2, d=16, prefix_len=5, n_chunks=3, chunk_len=9, pool_chunks=4,
+                      q_len=6)
+    out0, lse0 = run(w)
+    local = local_store_from_nope(w)
+    out1, lse1 = O.lazy_attention(w.q, w.q_start, w.q_pos0, local, local, w.chunks, w.chunk_start, w.num_q_heads,
+                                  w.num_kv_heads, w.head_dim, w.rope_base, w.causal, key_positions="local")
+    np.testing.assert_allclose(out1, out0, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse1, lse0, rtol=0, atol=1e-11)
+    # the materialised copies agree as well
+    m0 = O.materialize_k(w.pool, w.chunks, w.chunk_start, 2, 16, w.rope_base)
+    m1 = O.materialize_k(local, w.chunks, w.chunk_start, 2, 16, w.rope_base, key_positions="local")
+    for a, b in zip(m0, m1):
+        np.testing.assert_allclose(b, a, rtol=0, atol=1e-12)
+
+
+def test_local_store_bridge_identity_decode_with_capacity():
+    w = W.rag_decode(seed=22, batch=3, hq=6, hkv=2, d=16, n_chunks=3, chunk_len=12, pool_chunks=4, tail_len=5,
+                     tail_cap=9)
+    o0, l0 = O.lazy_decode(w.q, w.q_pos0, w.pool, w.pool, w.chunks, w.chunk_start, 6, 2, 16, w.rope_base)
+    local = local_store_from_nope(w)
+    o1, l1 = O.lazy_decode(w.q, w.q_pos0, local, local, w.chunks, w.chunk_start, 6, 2, 16, w.rope_base,
+                           key_positions="local")
+    np.testing.assert_allclose(o1, o0, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(l1, l0, rtol=0, atol=1e-11)
+
+
+def test_local_store_decode_rotates_query_by_relative_offset():
+    """Sec. 3.2 "Decoding": with local keys the query at m is rotated by m - Delta and meets the stored keys as they
+    are.  Brute force in pure Python (complex arithmetic) on lse, for two chunks at different offsets."""
+    d, base = 8, 1.0e4
+    reqs = [dict(chunks=[("a", 5, 30), ("b", 4, 7)], q_len=1, q_pos0=61)]
+    w = W.custom(23, 1, 1, d, base, reqs, kind="decode")
+    _, lse = O.lazy_decode(w.q, w.q_pos0, w.pool, w.pool, w.chunks, w.chunk_start, 1, 1, d, base,
+                           key_positions="local")
+    half = d // 2
+    th = [base ** (-2.0 * t / d) for t in range(half)]
+    q = [complex(float(w.q[0, 0, t]), float(w.q[0, 0, t + half])) for t in range(half)]
+    scores = []
+    for rec in w.chunks:
+        delta = int(rec["pos_offset"])
+        rel = int(w.q_pos0[0]) - delta
+        qr = [q[t] * cmath.exp(1j * rel * th[t]) for t in range(half)]
+        for j in range(int(rec["len"])):
+            a = int(rec["k_offset"]) + j * d
+            k = [complex(float(w.pool[a + t]), float(w.pool[a + t + half])) for t in range(half)]
+            scores.append(sum((qr[t].conjugate() * k[t]).real for t in range(half)) / math.sqrt(d))
+    mx = max(scores)
+    ref = mx + math.log(sum(math.exp(s - mx) for s in scores))
+    assert abs(lse[0, 0] - ref) < 1e-12
+
+
+def test_unknown_key_convention_is_rejected():
+    w = W.tiny_rag_prefill(seed=0)
+    with pytest.raises(ValueError):
+        run(w, key_positions="absolute")
