@@ -78,8 +78,24 @@ typedef struct lazy_attn_params {
   float softmax_scale;   /* 0 => 1/sqrt(D) (Eqn. standard attention) */
   const float* inv_freq; /* optional device array of D/2 fp32 frequencies theta_t (scaled / NTK tables) */
   int32_t num_splits;    /* 0 => chosen by the library; otherwise the number of KV splits per request */
-  int32_t reserved;      /* must be 0 */
+  int32_t key_positions; /* LAZY_KEYS_NOPE or LAZY_KEYS_LOCAL: how the chunk store holds its keys (below) */
 } lazy_attn_params_t;
+
+/*
+ * Key-store conventions (params->key_positions).  Values and the causal rule are the same in both; only the
+ * encoding of the stored keys differs.
+ *  LAZY_KEYS_NOPE  (0): keys are stored without positional encoding.  Key j of a record is rotated inside the
+ *                       kernels at pos_offset + j (prefill and decode rotate every key tile; the per-key angle is
+ *                       built from one base row per 32 keys and a 32-row table of offsets).
+ *  LAZY_KEYS_LOCAL (1): the paper's own convention (Sec. 3.2 "Prefilling": each document's cache keeps local
+ *                       positions from 0 and is reused at offset Delta with one fixed rotation).  Key j is stored
+ *                       already encoded at position j; using it at pos_offset + j needs the single rotation
+ *                       R(pos_offset), the same for every key of the record.  Prefill rotates each key tile by that
+ *                       one angle row; decode instead rotates the query by q_pos - pos_offset whenever the record
+ *                       changes (Sec. 3.2 "Decoding") and reads the keys as stored.
+ */
+#define LAZY_KEYS_NOPE 0
+#define LAZY_KEYS_LOCAL 1
 
 /*
  * Prefill (Sec. 3.2 "Prefilling"; Fig. 3(b)): every request's new query tokens attend over all keys of its chunk

@@ -19,7 +19,8 @@ int check_params(const lazy_attn_params_t* p) {
   if (p->causal != 0 && p->causal != 1) return LAZY_EINVAL;
   if (!isfinite(p->softmax_scale) || p->softmax_scale < 0.f) return LAZY_EINVAL;
   if (!p->inv_freq && !(isfinite(p->rope_base) && p->rope_base > 0.f)) return LAZY_EINVAL;
-  if (p->num_splits < 0 || p->reserved != 0) return LAZY_EINVAL;
+  if (p->num_splits < 0) return LAZY_EINVAL;
+  if (p->key_positions != LAZY_KEYS_NOPE && p->key_positions != LAZY_KEYS_LOCAL) return LAZY_EINVAL;
   if (p->head_dim != 64 && p->head_dim != 128) return LAZY_EUNSUPPORTED;
   return LAZY_OK;
 }
@@ -133,6 +134,7 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
   a.head_groups = 1;
   a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
+  a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
   return status(lazy::launch_prefill(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
 
@@ -177,6 +179,7 @@ int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const 
   a.head_groups = hg;
   a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
+  a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
   return status(lazy::launch_decode(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
 
@@ -253,7 +256,8 @@ int lazy_materialize_k(const lazy_attn_params_t* params, const void* k_pool, con
   return status(lazy::launch_materialize(static_cast<const uint16_t*>(k_pool), chunks, num_records, max_chunk_len,
                                          params->num_kv_heads, params->head_dim,
                                          params->inv_freq ? 0.0 : log2((double)params->rope_base),
-                                         params->inv_freq, static_cast<uint16_t*>(k_out), chunks_out,
+                                         params->inv_freq, params->key_positions == LAZY_KEYS_LOCAL,
+                                         static_cast<uint16_t*>(k_out), chunks_out,
                                          static_cast<hipStream_t>(stream)));
 }
 

@@ -32,6 +32,7 @@ struct AttnArgs {
   int32_t q_tiles;            // prefill: row tiles per (request, kv head)
   int32_t row_blocks;         // prefill: a workgroup covers 128 * row_blocks packed rows (2 = eight-wave kernel)
   int32_t head_groups;        // decode: ceil(group / 16)
+  int32_t local_keys;         // 1: the store holds keys encoded at local positions (LAZY_KEYS_LOCAL)
   double rope_log2_base;      // log2(rope_base), computed on the host (unused with inv_freq)
   float scale_log2;           // softmax scale * log2(e)
 };
@@ -48,6 +49,7 @@ hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int spl
                           uint16_t* out, float* lse, hipStream_t stream);
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
                               int max_chunk_len, int hkv, int head_dim, double rope_log2_base, const float* inv_freq,
+                              bool local_keys,
                               uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t stream);
 
 }  // namespace lazy

@@ -125,6 +125,18 @@ __device__ __forceinline__ void rotate_pair(float x1, float x2, float2 cb, float
   y2 = fmaf(x1, s, x2 * c);
 }
 
+// Rotate one pair by a single angle given its (cos, sin): the one rotation of a local-position key by its record's
+// offset.  Same fmaf form in every kernel that uses it.
+__device__ __forceinline__ void rotate_by(float x1, float x2, float2 cs, float& y1, float& y2) {
+  y1 = fmaf(x1, cs.x, -(x2 * cs.y));
+  y2 = fmaf(x1, cs.y, x2 * cs.x);
+}
+
+// Key handling of a kernel instance: keys already encoded at their positions (the plain kernels of the
+// materialise-then-attend baseline), NoPE keys rotated at pos_offset + j, or local-position keys (stored encoded at
+// j) rotated by the record's pos_offset.
+constexpr int kKeysPlain = 0, kKeysNope = 1, kKeysLocal = 2;
+
 // Rotate a query pair at position p (accurate angle per pair).
 __device__ __forceinline__ void rotate_q_pair(float x1, float x2, int p, double rev, float& y1, float& y2) {
   const float2 cs = rope_cs(p, rev);
@@ -344,9 +356,10 @@ __device__ __forceinline__ int kblk_t(int b) {
 // each rotating PP = D / (2 TPR) pairs of its row; V copied row-major in 16-byte chunks (VC per thread, of the same
 // row, so that a thread's share of K and V is one key row: threads 0..NT/2-1 hold rows 0..31).
 // The per-row cos/sin constants are written to a private LDS slice once per workgroup and read per tile.
-template <int D, bool ROT, int NT, bool CSD_REGS = false>
+template <int D, int KM, int NT, bool CSD_REGS = false>
 struct PLoader {
   using S = TileLayout<D>;
+  static constexpr bool ROT = KM != kKeysPlain, LOCAL = KM == kKeysLocal;
   static constexpr int TPR = NT / kSub;
   static constexpr int PP = D / (2 * TPR);
   static constexpr int NV = PP / 8;
@@ -355,7 +368,7 @@ struct PLoader {
   static_assert(VC * TPR == D / 8, "a row's V chunks are shared by its TPR threads");
   u32x4 klo[NV], khi[NV];
   u32x4 vr[VC];
-  float2 cdr[CSD_REGS && ROT ? PP : 1];
+  float2 cdr[CSD_REGS && KM == kKeysNope ? PP : 1];
   int tid, row, part;
 
   __device__ void init(int t) {
@@ -366,7 +379,7 @@ struct PLoader {
   // With CSD_REGS, after that barrier: keep this thread's per-row constants in registers (the loop writes LDS, so
   // they cannot be re-derived inside it).
   __device__ void load_constants(const float* csd) {
-    if (ROT && CSD_REGS) {
+    if (KM == kKeysNope && CSD_REGS) {
       const float* cd = csd + (row & (kAngleRows - 1)) * S::CSD_LD;
 #pragma unroll
       for (int e = 0; e < PP; ++e) cdr[e] = *reinterpret_cast<const float2*>(cd + cs_idx<D>(part * PP + e));
@@ -403,7 +416,8 @@ struct PLoader {
     }
   }
 
-  // cb: the tile's two base tables [2][CSW] (rows 0..31 and 32..63).
+  // cb: the tile's two base tables [2][CSW] (rows 0..31 and 32..63; for local-position keys both hold the record
+  // offset's angles and the per-row table is not used).
   __device__ void store(uint16_t* kbuf, uint16_t* vtbuf, const float* cb2, const float* csd) {
     uint16_t* krow = kbuf + row * S::KLD;
     const float* cb = cb2 + (row / kAngleRows) * S::CSW;
@@ -419,8 +433,12 @@ struct PLoader {
           const float x1 = (e & 1) ? bf_hi(klo[v][e >> 1]) : bf_lo(klo[v][e >> 1]);
           const float x2 = (e & 1) ? bf_hi(khi[v][e >> 1]) : bf_lo(khi[v][e >> 1]);
           const int ci = cs_idx<D>(t0 + e);
-          const float2 d = CSD_REGS ? cdr[8 * v + e] : *reinterpret_cast<const float2*>(cd + ci);
-          rotate_pair(x1, x2, *reinterpret_cast<const float2*>(cb + ci), d, yl[e], yh[e]);
+          if (LOCAL) {
+            rotate_by(x1, x2, *reinterpret_cast<const float2*>(cb + ci), yl[e], yh[e]);
+          } else {
+            const float2 d = CSD_REGS ? cdr[8 * v + e] : *reinterpret_cast<const float2*>(cd + ci);
+            rotate_pair(x1, x2, *reinterpret_cast<const float2*>(cb + ci), d, yl[e], yh[e]);
+          }
         }
         w0 = u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yh[0], yh[1]), pack2(yh[2], yh[3])};
         w1 = u32x4{pack2(yl[4], yl[5]), pack2(yl[6], yl[7]), pack2(yh[4], yh[5]), pack2(yh[6], yh[7])};
@@ -437,11 +455,13 @@ struct PLoader {
 };
 
 // Base tables of a 64-key tile whose first key sits at position b0: [0] for rows 0..31, [1] for rows 32..63.
-template <int D>
+// For local-position keys b0 is the record offset and both halves get its angles.
+template <int D, bool LOCAL>
 __device__ __forceinline__ void prefill_base(float* csb2, const double* freq, int tid, int b0) {
   if (tid < D) {
     const int h = tid / (D / 2), t = tid % (D / 2);
-    *reinterpret_cast<float2*>(csb2 + h * TileLayout<D>::CSW + cs_idx<D>(t)) = rope_cs(b0 + kAngleRows * h, freq[t]);
+    *reinterpret_cast<float2*>(csb2 + h * TileLayout<D>::CSW + cs_idx<D>(t)) =
+        rope_cs(LOCAL ? b0 : b0 + kAngleRows * h, freq[t]);
   }
 }
 
@@ -576,10 +596,11 @@ __device__ __forceinline__ void attend_tile(const uint16_t* kb, const uint16_t* 
   __builtin_amdgcn_s_setprio(0);
 }
 
-template <int D, bool ROT, int NW, int NBUF, int RB>
+template <int D, int KM, int NW, int NBUF, int RB>
 __global__ __launch_bounds__(NW * 64)
 __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void prefill_kernel(AttnArgs a) {
   __shared__ PrefillSmem<D, NBUF> sm;
+  constexpr bool ROT = KM != kKeysPlain, LOCAL = KM == kKeysLocal;
   using S = TileLayout<D>;
   constexpr int NT = NW * 64;
   constexpr int BM = 32 * NW * RB;
@@ -627,7 +648,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
       }
     }
   }
-  PLoader<D, ROT, NT, RB == 2> ld;
+  PLoader<D, KM, NT, RB == 2> ld;
   ld.init(tid);
   TileIter<kSub> it;
   it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
@@ -677,10 +698,11 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   TileIter<kSub> ahead = it;
   bool have_ahead = false;
   if (have && NBUF == 2) {
-    if (ROT) prefill_base<D>(sm.csb[0][0], sm.freq, tid, it.cur.pos + it.j0);
+    if (ROT) prefill_base<D, LOCAL>(sm.csb[0][0], sm.freq, tid, it.cur.pos + (LOCAL ? 0 : it.j0));
     ahead.step();
     have_ahead = ahead.seek(a.causal, qmax);
-    if (ROT && have_ahead) prefill_base<D>(sm.csb[1][0], sm.freq, tid, ahead.cur.pos + ahead.j0);
+    if (ROT && have_ahead)
+      prefill_base<D, LOCAL>(sm.csb[1][0], sm.freq, tid, ahead.cur.pos + (LOCAL ? 0 : ahead.j0));
     __syncthreads();
     ld.store(sm.k[0], sm.v[0], sm.csb[0][0], sm.csd);
     __syncthreads();
@@ -688,13 +710,13 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   int parity = 0;
   while (have) {
     const int nvalid = min(kSub, it.cur.len - it.j0);
-    const int b0 = it.cur.pos + it.j0;
+    const int b0 = it.cur.pos + it.j0, rec_pos = it.cur.pos;
     int cur_buf = 0;
     bool have_next;
     if (NBUF == 1) {
       it.step();
       have_next = it.seek(a.causal, qmax);
-      if (ROT) prefill_base<D>(sm.csb[0][0], sm.freq, tid, b0);
+      if (ROT) prefill_base<D, LOCAL>(sm.csb[0][0], sm.freq, tid, LOCAL ? rec_pos : b0);
       __syncthreads();
       ld.store(sm.k[0], sm.v[0], sm.csb[0][0], sm.csd);
       __syncthreads();
@@ -715,7 +737,8 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     attend_tile<D, NT, RB>(sm.k[cur_buf], sm.v[cur_buf], lane, qf, o, m2, lsum, qpos, b0, nvalid, qmin, a.causal, c);
     if (NBUF == 2) {
       // Base angles two tiles ahead go to the table slot this tile used; the next tile goes to the other buffer.
-      if (ROT && have_ahead) prefill_base<D>(sm.csb[parity][0], sm.freq, tid, ahead.cur.pos + ahead.j0);
+      if (ROT && have_ahead)
+        prefill_base<D, LOCAL>(sm.csb[parity][0], sm.freq, tid, ahead.cur.pos + (LOCAL ? 0 : ahead.j0));
       if (have_next) ld.store(sm.k[parity ^ 1], sm.v[parity ^ 1], sm.csb[parity ^ 1][0], sm.csd);
       __syncthreads();
       parity ^= 1;
@@ -771,6 +794,7 @@ struct DecodeSmem {
   uint16_t v[4][kDecWaveKeys * VLD] __attribute__((aligned(16)));
   float csd[kDecWaveKeys * CSD_LD] __attribute__((aligned(16)));
   float csb[4][2][CSB] __attribute__((aligned(16)));
+  u32x4 qsave[D / 64][2][64];                       // raw Q fragments [s][half][lane] (local-position keys)
   double freq[D / 2];
 };
 template <int D>
@@ -830,9 +854,13 @@ __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, 
   }
 }
 
-template <int D, bool ROT>
+template <int D, int KM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_kernel(AttnArgs a) {
   __shared__ DecodeSmem<D> sm;
+  // Keys are rotated in registers only for a NoPE store; with local-position keys the query is rotated by the
+  // relative offset q_pos - pos_offset whenever the record changes (Sec. 3.2 "Decoding") and the keys are used as
+  // stored.
+  constexpr bool ROT = KM == kKeysNope, LOCAL = KM == kKeysLocal;
   using S = DecodeSmem<D>;
   constexpr int SP = DecTile<D>::SP;
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
@@ -882,22 +910,35 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     if (have && lane < D / 2)
       *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
   }
-  // Q fragments in the decode head-dimension order, rotated at the query position.
+  // Q fragments in the decode head-dimension order, rotated at the query position.  With local-position keys they
+  // are built per record instead (below), from the raw query.
   bf16x8 qf[D / 32];
+  if (!LOCAL) {
 #pragma unroll
-  for (int s = 0; s < SP; ++s) {
-    float y1[8], y2[8];
-    const int t0 = 32 * s + 8 * kq;
+    for (int s = 0; s < SP; ++s) {
+      float y1[8], y2[8];
+      const int t0 = 32 * s + 8 * kq;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float x1 = (e & 1) ? bf_hi(qraw[s][0][e >> 1]) : bf_lo(qraw[s][0][e >> 1]);
-      const float x2 = (e & 1) ? bf_hi(qraw[s][1][e >> 1]) : bf_lo(qraw[s][1][e >> 1]);
-      rotate_q_pair(x1, x2, qpos, sm.freq[t0 + e], y1[e], y2[e]);
+      for (int e = 0; e < 8; ++e) {
+        const float x1 = (e & 1) ? bf_hi(qraw[s][0][e >> 1]) : bf_lo(qraw[s][0][e >> 1]);
+        const float x2 = (e & 1) ? bf_hi(qraw[s][1][e >> 1]) : bf_lo(qraw[s][1][e >> 1]);
+        rotate_q_pair(x1, x2, qpos, sm.freq[t0 + e], y1[e], y2[e]);
+      }
+      qf[2 * s] =
+          as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])});
+      qf[2 * s + 1] =
+          as_bf16x8(u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])});
     }
-    qf[2 * s] = as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])});
-    qf[2 * s + 1] = as_bf16x8(u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])});
   }
-  __syncthreads();  // per-row table complete
+  if (LOCAL && wave == 0) {
+#pragma unroll
+    for (int s = 0; s < SP; ++s) {
+      sm.qsave[s][0][lane] = qraw[s][0];
+      sm.qsave[s][1][lane] = qraw[s][1];
+    }
+  }
+  int qdelta = -1;  // record offset the fragments are rotated for (local-position keys; offsets are >= 0)
+  __syncthreads();  // per-row table and saved Q complete
 
   f32x4 o[D / 16];
 #pragma unroll
@@ -915,6 +956,29 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   while (have) {
     const int nvalid = min(kDecWaveKeys, it.cur.len - it.j0);
     const int b0 = it.cur.pos + it.j0;
+    if (LOCAL && it.cur.pos != qdelta) {
+      // New record: q' = R(q_pos - pos_offset) q, one rotation by the relative offset.  One lane per pair writes the
+      // angle row to this wave's table (same-wave LDS ordering: written here, read just below).
+      qdelta = it.cur.pos;
+      if (lane < D / 2)
+        *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(qpos - qdelta, sm.freq[lane]);
+#pragma unroll
+      for (int s = 0; s < SP; ++s) {
+        float y1[8], y2[8];
+        const u32x4 ql = sm.qsave[s][0][lane], qh = sm.qsave[s][1][lane];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x1 = (e & 1) ? bf_hi(ql[e >> 1]) : bf_lo(ql[e >> 1]);
+          const float x2 = (e & 1) ? bf_hi(qh[e >> 1]) : bf_lo(qh[e >> 1]);
+          rotate_by(x1, x2, *reinterpret_cast<const float2*>(sm.csb[wave][0] + csb_idx<D>(32 * s + 8 * kq + e)),
+                    y1[e], y2[e]);
+        }
+        qf[2 * s] =
+            as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])});
+        qf[2 * s + 1] =
+            as_bf16x8(u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])});
+      }
+    }
     for (int k = 0; k < 4 && it.left > 0; ++k) it.step();
     const bool have_next = it.seek(a.causal, qpos);
     if (have_next) {
@@ -1162,7 +1226,7 @@ __global__ __launch_bounds__(kThreads) void materialize_plan_kernel(const lazy_c
 
 // Rotate-and-copy: workgroup = (64-key sub-tile, KV head, record).  Same angle decomposition and rounding as the
 // lazy loader, written back in the natural head-dimension order.
-template <int D>
+template <int D, bool LOCAL>
 __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint16_t* __restrict__ k_pool,
                                                                       const lazy_chunk_t* __restrict__ in,
                                                                       const lazy_chunk_t* __restrict__ plan,
@@ -1177,7 +1241,10 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
   if (j0 >= rc.len) return;
   if (tid < D / 2) freq[tid] = theta_rev(tid, D, log2_base, inv_freq);
   __syncthreads();
-  if (tid < D) cs[tid / (D / 2)][tid % (D / 2)] = rope_cs(rc.pos + j0 + kAngleRows * (tid / (D / 2)), freq[tid % (D / 2)]);
+  // NoPE keys: base angles of the two 32-row halves (key j at rc.pos + j); local-position keys: the record offset.
+  if (tid < D)
+    cs[tid / (D / 2)][tid % (D / 2)] =
+        rope_cs(LOCAL ? rc.pos : rc.pos + j0 + kAngleRows * (tid / (D / 2)), freq[tid % (D / 2)]);
   __syncthreads();
   const int row = tid >> 2, quarter = tid & 3;
   if (j0 + row >= rc.len) return;
@@ -1193,7 +1260,10 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
     for (int e = 0; e < 8; ++e) {
       const float x1 = (e & 1) ? bf_hi(wl[e >> 1]) : bf_lo(wl[e >> 1]);
       const float x2 = (e & 1) ? bf_hi(wh[e >> 1]) : bf_lo(wh[e >> 1]);
-      rotate_pair(x1, x2, cs[row / kAngleRows][t0 + e], rope_cs(row % kAngleRows, freq[t0 + e]), yl[e], yh[e]);
+      if (LOCAL)
+        rotate_by(x1, x2, cs[0][t0 + e], yl[e], yh[e]);
+      else
+        rotate_pair(x1, x2, cs[row / kAngleRows][t0 + e], rope_cs(row % kAngleRows, freq[t0 + e]), yl[e], yh[e]);
     }
     *reinterpret_cast<u32x4*>(dst + t0) =
         u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yl[4], yl[5]), pack2(yl[6], yl[7])};
@@ -1206,25 +1276,40 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
 #ifndef LAZY_PREFILL_BIG_WAVES
 #define LAZY_PREFILL_BIG_WAVES 8
 #endif
-template <int D, bool ROT>
+template <int D, int KM>
 hipError_t prefill_d(const AttnArgs& a, hipStream_t st) {
   const dim3 grid(a.q_tiles, a.hkv, a.batch * a.splits);
   if constexpr (D == 128) {
     if (a.row_blocks == 2) {
-      hipLaunchKernelGGL((prefill_kernel<D, ROT, LAZY_PREFILL_BIG_WAVES, 2, 8 / LAZY_PREFILL_BIG_WAVES>), grid,
+      hipLaunchKernelGGL((prefill_kernel<D, KM, LAZY_PREFILL_BIG_WAVES, 2, 8 / LAZY_PREFILL_BIG_WAVES>), grid,
                          dim3(64 * LAZY_PREFILL_BIG_WAVES), 0, st, a);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((prefill_kernel<D, ROT, 4, 1, 1>), grid, dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((prefill_kernel<D, KM, 4, 1, 1>), grid, dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 
-template <int D, bool ROT>
+template <int D, int KM>
 hipError_t decode_d(const AttnArgs& a, hipStream_t st) {
   const dim3 grid(a.splits, a.hkv * a.head_groups, a.batch);
-  hipLaunchKernelGGL((decode_kernel<D, ROT>), grid, dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((decode_kernel<D, KM>), grid, dim3(kThreads), 0, st, a);
   return hipGetLastError();
+}
+
+int key_mode(const AttnArgs& a, bool rotate_k) { return !rotate_k ? kKeysPlain : a.local_keys ? kKeysLocal : kKeysNope; }
+
+template <int D>
+hipError_t prefill_dk(const AttnArgs& a, int km, hipStream_t st) {
+  return km == kKeysPlain ? prefill_d<D, kKeysPlain>(a, st)
+         : km == kKeysNope ? prefill_d<D, kKeysNope>(a, st)
+                           : prefill_d<D, kKeysLocal>(a, st);
+}
+template <int D>
+hipError_t decode_dk(const AttnArgs& a, int km, hipStream_t st) {
+  return km == kKeysPlain ? decode_d<D, kKeysPlain>(a, st)
+         : km == kKeysNope ? decode_d<D, kKeysNope>(a, st)
+                           : decode_d<D, kKeysLocal>(a, st);
 }
 
 }  // namespace
@@ -1242,40 +1327,43 @@ hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int spl
 }
 
 hipError_t launch_prefill(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t st) {
-  hipError_t e;
-  if (head_dim == 128)
-    e = rotate_k ? prefill_d<128, true>(a, st) : prefill_d<128, false>(a, st);
-  else
-    e = rotate_k ? prefill_d<64, true>(a, st) : prefill_d<64, false>(a, st);
+  const int km = key_mode(a, rotate_k);
+  const hipError_t e = head_dim == 128 ? prefill_dk<128>(a, km, st) : prefill_dk<64>(a, km, st);
   if (e != hipSuccess || a.splits == 1) return e;
   return launch_combine(a.ws_o, a.ws_lse, a.splits, a.total_q * a.hq, head_dim, a.out, a.lse, st);
 }
 
 hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t st) {
-  hipError_t e;
-  if (head_dim == 128)
-    e = rotate_k ? decode_d<128, true>(a, st) : decode_d<128, false>(a, st);
-  else
-    e = rotate_k ? decode_d<64, true>(a, st) : decode_d<64, false>(a, st);
+  const int km = key_mode(a, rotate_k);
+  const hipError_t e = head_dim == 128 ? decode_dk<128>(a, km, st) : decode_dk<64>(a, km, st);
   if (e != hipSuccess || a.splits == 1) return e;
   return launch_combine(a.ws_o, a.ws_lse, a.splits, a.total_q * a.hq, head_dim, a.out, a.lse, st);
 }
 
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
                               int max_chunk_len, int hkv, int head_dim, double rope_log2_base, const float* inv_freq,
-                              uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t st) {
+                              bool local_keys, uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t st) {
   if (num_records <= 0) return hipSuccess;
   hipLaunchKernelGGL(materialize_plan_kernel, dim3(1), dim3(kThreads), 0, st, chunks, num_records, hkv, head_dim,
                      chunks_out);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_chunk_len <= 0) return e;
   const dim3 grid((max_chunk_len + kSub - 1) / kSub, hkv, num_records);
-  if (head_dim == 128)
-    hipLaunchKernelGGL(materialize_rotate_kernel<128>, grid, dim3(kThreads), 0, st, k_pool, chunks, chunks_out,
-                       rope_log2_base, inv_freq, k_out);
-  else
-    hipLaunchKernelGGL(materialize_rotate_kernel<64>, grid, dim3(kThreads), 0, st, k_pool, chunks, chunks_out,
-                       rope_log2_base, inv_freq, k_out);
+  if (head_dim == 128) {
+    if (local_keys)
+      hipLaunchKernelGGL((materialize_rotate_kernel<128, true>), grid, dim3(kThreads), 0, st, k_pool, chunks,
+                         chunks_out, rope_log2_base, inv_freq, k_out);
+    else
+      hipLaunchKernelGGL((materialize_rotate_kernel<128, false>), grid, dim3(kThreads), 0, st, k_pool, chunks,
+                         chunks_out, rope_log2_base, inv_freq, k_out);
+  } else {
+    if (local_keys)
+      hipLaunchKernelGGL((materialize_rotate_kernel<64, true>), grid, dim3(kThreads), 0, st, k_pool, chunks,
+                         chunks_out, rope_log2_base, inv_freq, k_out);
+    else
+      hipLaunchKernelGGL((materialize_rotate_kernel<64, false>), grid, dim3(kThreads), 0, st, k_pool, chunks,
+                         chunks_out, rope_log2_base, inv_freq, k_out);
+  }
   return hipGetLastError();
 }
 

@@ -17,6 +17,7 @@ from .workloads import CHUNK_DTYPE, Workload, bf16_bits
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblazyattn.so")
 
 LAZY_OK, LAZY_EINVAL, LAZY_EUNSUPPORTED, LAZY_EWORKSPACE, LAZY_EHIP, LAZY_EDATA = 0, -1, -2, -3, -4, -5
+KEYS_NOPE, KEYS_LOCAL = 0, 1  # key-store conventions (lazy_attn_params_t.key_positions)
 
 _c_i32, _c_i64, _c_f32, _c_p, _c_sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -31,7 +32,7 @@ class LazyAttnParams(ctypes.Structure):
         ("softmax_scale", _c_f32),
         ("inv_freq", _c_p),
         ("num_splits", _c_i32),
-        ("reserved", _c_i32),
+        ("key_positions", _c_i32),
     ]
 
 
@@ -107,11 +108,13 @@ class Config:
     softmax_scale: float = 0.0
     inv_freq: torch.Tensor | None = None  # device fp32 [D/2]
     num_splits: int = 0
+    key_positions: int = 0  # KEYS_NOPE or KEYS_LOCAL
 
     def c(self) -> LazyAttnParams:
         return LazyAttnParams(self.num_q_heads, self.num_kv_heads, self.head_dim, int(bool(self.causal)),
                               float(self.rope_base), float(self.softmax_scale),
-                              None if self.inv_freq is None else self.inv_freq.data_ptr(), int(self.num_splits), 0)
+                              None if self.inv_freq is None else self.inv_freq.data_ptr(), int(self.num_splits),
+                              int(self.key_positions))
 
 
 def config_of(w: Workload, **kw) -> Config:

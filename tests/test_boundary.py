@@ -55,7 +55,7 @@ def test_struct_layout_matches_header(tmp_path, ops):
         " offsetof(lazy_chunk_t, len), offsetof(lazy_chunk_t, pos_offset), offsetof(lazy_chunk_t, k_stride),"
         " offsetof(lazy_chunk_t, v_stride), sizeof(lazy_attn_params_t));"
         'printf("%zu %zu %zu %zu\\n", offsetof(lazy_attn_params_t, rope_base), offsetof(lazy_attn_params_t, inv_freq),'
-        " offsetof(lazy_attn_params_t, num_splits), offsetof(lazy_attn_params_t, reserved));"
+        " offsetof(lazy_attn_params_t, num_splits), offsetof(lazy_attn_params_t, key_positions));"
         "return 0;}"
     )
     exe = tmp_path / "layout"
@@ -66,7 +66,7 @@ def test_struct_layout_matches_header(tmp_path, ops):
     LC, LP = ops.LazyChunk, ops.LazyAttnParams
     assert c == [ctypes.sizeof(LC), LC.v_offset.offset, LC.len.offset, LC.pos_offset.offset, LC.k_stride.offset,
                  LC.v_stride.offset, ctypes.sizeof(LP)]
-    assert p == [LP.rope_base.offset, LP.inv_freq.offset, LP.num_splits.offset, LP.reserved.offset]
+    assert p == [LP.rope_base.offset, LP.inv_freq.offset, LP.num_splits.offset, LP.key_positions.offset]
     dt = W.CHUNK_DTYPE
     assert [dt.fields[n][1] for n in ("k_offset", "v_offset", "len", "pos_offset", "k_stride", "v_stride")] == [
         0, c[1], c[2], c[3], c[4], c[5]]
@@ -139,7 +139,8 @@ def test_scalar_argument_errors_return_before_any_launch(ops):
     assert prefill(P(8, 2, 128, 1, -1.0, 0.0, None, 0, 0)) == ops.LAZY_EINVAL         # rope base
     assert prefill(P(8, 2, 128, 1, 1e4, -0.5, None, 0, 0)) == ops.LAZY_EINVAL         # softmax scale
     assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, -1, 0)) == ops.LAZY_EINVAL         # splits
-    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 7)) == ops.LAZY_EINVAL          # reserved
+    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 7)) == ops.LAZY_EINVAL          # key convention
+    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, -1)) == ops.LAZY_EINVAL
     assert prefill(good, batch=-1) == ops.LAZY_EINVAL
     assert prefill(good, batch=0) == ops.LAZY_OK                                       # nothing to do
     assert prefill(good, total_q=0) == ops.LAZY_OK

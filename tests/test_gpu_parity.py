@@ -71,6 +71,8 @@ def run_and_check(w, tag, cfg_kw=None, requests=None):
     okw = {}
     if cfg_kw and cfg_kw.get("softmax_scale"):
         okw["softmax_scale"] = cfg_kw["softmax_scale"]
+    if cfg_kw and cfg_kw.get("key_positions") == ops.KEYS_LOCAL:
+        okw["key_positions"] = "local"
     ref_o, ref_l = oracle(w, requests=requests, **okw)
     rows = None if requests is None else rows_of(w, requests)
     assert_close(out, lse, ref_o, ref_l, rows, tag)
@@ -286,3 +288,97 @@ def test_full_size_sampled(name):
     w = make()
     print(f"{name}: batch={w.batch} total_q={w.total_q} max_kv={w.max_kv_len} meta={w.meta}", flush=True)
     run_and_check(w, "full " + name, requests=reqs)
+
+
+# --------------------------------------------------------------------------------------------------------------
+# Local-position key stores (LAZY_KEYS_LOCAL): the same random pools, read as keys already encoded at their local
+# index j; the oracle applies the one rotation by pos_offset (its pins: test_oracle.py, local-store section).
+LOCAL = dict(key_positions=ops.KEYS_LOCAL)
+
+
+@pytest.mark.parametrize("name", ["rag_d128_g4", "rag_d64_g2_split3", "rag_d128_g1_split1", "varlen_g7", "icl_small"])
+def test_local_key_store_prefill_matches_oracle(name):
+    fn, kw, ckw = PREFILL_CASES[name]
+    run_and_check(fn(**kw), "local " + name, {**ckw, **LOCAL})
+
+
+@pytest.mark.parametrize("name", list(DECODE_CASES))
+def test_local_key_store_decode_matches_oracle(name):
+    kw, ckw = DECODE_CASES[name]
+    run_and_check(W.rag_decode(**kw), "local decode " + name, {**ckw, **LOCAL})
+
+
+def test_local_key_store_decode_many_short_records():
+    """Decode re-rotates the query at every record change: 40 records of 1..70 keys (partial tiles, records shorter
+    than a tile, waves that cross several records per tile step), non-causal as well."""
+    rng = np.random.default_rng(91)
+    reqs = []
+    for r in range(3):
+        pos, ch = 0, []
+        for i in range(40):
+            n = int(rng.integers(1, 71))
+            ch.append((n, pos + int(rng.integers(0, 5))))
+            pos = ch[-1][1] + n
+        reqs.append(dict(chunks=ch, q_len=1, q_pos0=pos + 3))
+    w = W.custom(92, 8, 2, 128, 5e5, reqs, kind="decode")
+    run_and_check(w, "local decode short records", LOCAL)
+    w.causal = False
+    run_and_check(w, "local decode short records non-causal", LOCAL)
+
+
+def test_local_lazy_prefill_equals_materialize_then_attend_bitwise():
+    w = W.rag_prefill(seed=93, batch=3, hq=8, hkv=2, d=128, prefix_len=30, n_chunks=3, chunk_len=150, pool_chunks=5,
+                      q_len=70)
+    dw = ops.upload(w)
+    cfg = ops.config_of(w, **LOCAL)
+    out_l, lse_l = ops.run_lazy(dw, cfg)
+    (out_m, lse_m), _ = ops.run_materialized(dw, cfg)
+    torch.cuda.synchronize()
+    assert torch.equal(out_l.view(torch.int16), out_m.view(torch.int16))
+    assert torch.equal(lse_l, lse_m)
+
+
+def test_local_materialized_keys_match_oracle():
+    w = W.rag_prefill(seed=94, batch=2, hq=4, hkv=2, d=128, prefix_len=10, n_chunks=2, chunk_len=77, pool_chunks=3,
+                      q_len=5)
+    dw = ops.upload(w)
+    cfg = ops.config_of(w, **LOCAL)
+    total = int(w.chunks["len"].astype(np.int64).sum())
+    k_out, ch_out = ops.materialize_k(cfg, dw.pool, dw.chunks, int(w.chunks["len"].max()), total)
+    torch.cuda.synchronize()
+    recs = ops.chunks_from_tensor(ch_out)
+    ref = O.materialize_k(w.pool, w.chunks, w.chunk_start, 2, 128, w.rope_base, key_positions="local")
+    got = k_out.float().cpu().numpy()
+    for r in range(w.batch):
+        start = 0
+        for i in range(int(w.chunk_start[r]), int(w.chunk_start[r + 1])):
+            n = int(recs[i]["len"])
+            blk = got[int(recs[i]["k_offset"]): int(recs[i]["k_offset"]) + 2 * n * 128].reshape(2, n, 128)
+            np.testing.assert_allclose(blk, ref[r][:, start:start + n], rtol=2 ** -8, atol=1e-5)
+            start += n
+
+
+def test_local_key_store_position_discrimination():
+    """As test_position_discrimination, for the local-position convention (prefill and decode)."""
+    reqs = [dict(chunks=[(24, 5 + 37 * r), (24, 300 + 11 * r), (4, 400 + 3 * r)], q_len=4, q_pos0=400 + 3 * r)
+            for r in range(4)]
+    w = W.custom(95, 4, 2, 128, 1e4, reqs)
+    for kind in ("prefill", "decode"):
+        if kind == "decode":
+            w = W.custom(96, 4, 2, 128, 1e4, [dict(chunks=c["chunks"], q_len=1, q_pos0=c["q_pos0"] + 3)
+                                               for c in reqs], kind="decode")
+        dw = ops.upload(w)
+        out, _ = ops.run_lazy(dw, ops.config_of(w, **LOCAL))
+        torch.cuda.synchronize()
+        o = out.float().cpu().numpy()
+        ref, _ = oracle(w, key_positions="local")
+        for i in range(len(w.chunks)):
+            r = int(np.searchsorted(w.chunk_start, i, side="right")) - 1
+            rows = slice(int(w.q_start[r]), int(w.q_start[r + 1]))
+            e0 = np.abs(o[rows] - ref[rows]).mean()
+            for d in (-1, 1):
+                w2 = W.Workload(**{**w.__dict__})
+                w2.chunks = w.chunks.copy()
+                w2.chunks["pos_offset"][i] += d
+                e1 = np.abs(o[rows] - oracle(w2, key_positions="local")[0][rows]).mean()
+                assert e1 > 8 * e0, (kind, i, d, e0, e1)
