@@ -345,6 +345,13 @@ def main() -> int:
                                          dp.chunk_start, wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws,
                                          plain=True), args.steps, args.warmup)
 
+    # The same batch over a local-position key store (keys kept encoded at their local index; one rotation per
+    # record offset).  The pool's values are read as such keys: same shapes and traffic.
+    cfg_local = ops.config_of(wp, key_positions=ops.KEYS_LOCAL)
+    local_ms = timed(lambda: ops.prefill(cfg_local, dp.q, dp.q_start, dp.q_pos0, dp.pool, dp.pool, dp.chunks,
+                                         dp.chunk_start, wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws),
+                     args.steps, args.warmup)
+
     # Materialise-then-attend baseline: rotate-and-copy K, then plain attention over the copy.
     total_kv = int(wp.chunks["len"].astype(np.int64).sum())
     k_mat = torch.empty(cfg.num_kv_heads * total_kv * cfg.head_dim, dtype=torch.bfloat16, device=dev)
@@ -401,6 +408,8 @@ def main() -> int:
             "logical_hbm_gbps": round(alg_bytes / (ms * 1e-3) / 1e9, 1),
             "no_rotation_ms": round(norot_ms, 5),
             "rotation_overhead": round(ms / norot_ms - 1.0, 4),
+            "local_keys_ms": round(local_ms, 5),
+            "local_keys_tflops": round(flops / (local_ms * 1e-3) / 1e12, 3),
             "materialize_ms": round(mat_ms, 5),
             "plain_attention_ms": round(plain_ms, 5),
             "materialize_then_attend_ms": round(mat_ms + plain_ms, 5),
@@ -428,6 +437,9 @@ def main() -> int:
         dnorot = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
                                           wd.max_kv_len, out=outd, lse=lsed, workspace=wsd, plain=True),
                        args.steps, args.warmup)
+        cfgd_local = ops.config_of(wd, key_positions=ops.KEYS_LOCAL)
+        dlocal = timed(lambda: ops.decode(cfgd_local, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
+                                          wd.max_kv_len, out=outd, lse=lsed, workspace=wsd), args.steps, args.warmup)
         tkv = int(wd.chunks["len"].astype(np.int64).sum())
         kmd = torch.empty(cfgd.num_kv_heads * tkv * cfgd.head_dim, dtype=torch.bfloat16, device=dev)
         chd = torch.empty_like(dd.chunks)
@@ -448,6 +460,8 @@ def main() -> int:
             "splits": int(wsd_bytes // (wd.batch * wd.num_q_heads * (2 * wd.head_dim + 4))) if wsd_bytes else 1,
             "no_rotation_ms": round(dnorot, 5),
             "rotation_overhead": round(dms / dnorot - 1.0, 4),
+            "local_keys_ms": round(dlocal, 5),
+            "local_keys_logical_hbm_gbps": round(dbytes / (dlocal * 1e-3) / 1e9, 1),
             "materialize_ms": round(dmat, 5),
             "plain_decode_ms": round(dplain, 5),
             "materialize_then_attend_ms": round(dmat + dplain, 5),

@@ -179,6 +179,67 @@ LAZY_API int lazy_plain_attn_decode(const lazy_attn_params_t* params, const void
                            void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Chunk-major shared decode.  Position-free storage lets one stored chunk serve several requests of a batch at
+ * different offsets (the problem statement at the start of Sec. 3).  In decode, where reading K/V dominates
+ * (Sec. 3.2 "Decoding"), such a batch can read every shared chunk once per step for all of its users instead of
+ * once per user.  A work item is one key range of one stored chunk together with up to floor(16 / G) of its users
+ * (G = num_q_heads / num_kv_heads <= 16); its workgroups (one per KV head) read the range once and score it
+ * against every (user, query head) pair.  User u's query is rotated by the relative offset q_pos[r_u] - pos_offset_u
+ * (the query-side rotation of Sec. 3.2 "Decoding"); keys are used at their local index j: as stored for a
+ * local-position store, rotated by R(j) for a NoPE store, since (R(q_pos) q).(R(pos_offset + j) k) =
+ * (R(q_pos - pos_offset) q).(R(j) k) (the relative-rotation Fact of Sec. 3.2).  The causal rule is applied per
+ * user (key j visible iff pos_offset_u + j <= q_pos[r_u]).  Every (user, item) writes one partial result into its
+ * request's slot; the request's slots are then merged as in lazy_attn_combine.
+ */
+typedef struct lazy_shared_item {
+  int64_t k_offset;   /* the stored chunk, as in lazy_chunk_t */
+  int64_t v_offset;
+  int32_t k_stride;
+  int32_t v_stride;
+  int32_t key_begin;  /* this item covers the chunk's keys key_begin .. key_end - 1 */
+  int32_t key_end;
+  int32_t user_begin; /* its users are users[user_begin .. user_begin + num_users - 1] */
+  int32_t num_users;  /* 1 .. floor(16 / G) */
+} lazy_shared_item_t; /* 40 bytes */
+
+typedef struct lazy_shared_user {
+  int32_t request;    /* the request: row block of q, q_pos and out */
+  int32_t pos_offset; /* the chunk's offset in that request */
+  int32_t slot;       /* partial-result slot within the request, 0 .. (slot_start[r+1] - slot_start[r]) - 1 */
+  int32_t reserved;   /* 0 */
+} lazy_shared_user_t; /* 16 bytes */
+
+/*
+ * Host planner (CPU only, on HOST copies of the decode tables): groups the records that read the same stored keys
+ * (same k_offset, v_offset, k_stride, v_stride) and cuts each record into pieces of at most max_keys_per_item keys
+ * (0 = 1024).  Each piece of each record is one (user, item) pair; pieces of one stored range with the same bounds
+ * share items.  Items are ordered by key count, longest first.  Writes *num_items items, *num_users users and
+ * slot_start[batch+1] (prefix sums of the slots per request).  Returns LAZY_EINVAL if a capacity is too small (the
+ * counts needed are still written), LAZY_EUNSUPPORTED if G > 16, LAZY_EDATA for a negative length.
+ */
+LAZY_API int lazy_shared_decode_plan(const lazy_attn_params_t* params, const lazy_chunk_t* chunks,
+                                     const int32_t* chunk_start, int32_t batch, int32_t max_keys_per_item,
+                                     lazy_shared_item_t* items, int32_t item_capacity, lazy_shared_user_t* users,
+                                     int32_t user_capacity, int32_t* num_items, int32_t* num_users,
+                                     int32_t* slot_start);
+
+/*
+ * Shared decode over a plan (all arrays in device memory): q [batch][Hq][D] bf16, q_pos [batch] int32, items /
+ * users / slot_start as written by lazy_shared_decode_plan, max_slots >= the largest slot count of a request.
+ * out [batch][Hq][D] bf16 and lse [batch][Hq] (or NULL) as for lazy_attn_decode.  workspace: at least
+ * lazy_attn_decode_shared_workspace_size(params, batch, max_slots) bytes, holding the partial results
+ * [max_slots][batch * Hq] (bf16 outputs, then fp32 log-sum-exps).  Requests with no slot get out = 0, lse = -inf.
+ */
+LAZY_API int lazy_attn_decode_shared(const lazy_attn_params_t* params, const void* q, const int32_t* q_pos,
+                                     const void* k_pool, const void* v_pool, const lazy_shared_item_t* items,
+                                     int32_t num_items, const lazy_shared_user_t* users, const int32_t* slot_start,
+                                     int32_t batch, int32_t max_slots, void* out, float* lse, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
+LAZY_API size_t lazy_attn_decode_shared_workspace_size(const lazy_attn_params_t* params, int32_t batch,
+                                                       int32_t max_slots);
+
+/*
  * Host-side check of the table contents against the layout contract, on HOST copies of the tables (CPU only, no
  * device access).  k_pool_elems / v_pool_elems are the pool sizes in elements.  Returns LAZY_OK or LAZY_EDATA and
  * writes the offending record / request index and a reason to *bad_index / reason (either may be NULL).

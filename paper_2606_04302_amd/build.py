@@ -34,6 +34,7 @@ SOURCES = [
     ("lazy_attn_kernels.hip", "hip"),
     ("lazy_attn_api.cpp", "hip"),
     ("lazy_attn_validate.cpp", "host"),
+    ("lazy_attn_plan.cpp", "host"),
 ]
 
 

@@ -261,6 +261,51 @@ int lazy_materialize_k(const lazy_attn_params_t* params, const void* k_pool, con
                                          static_cast<hipStream_t>(stream)));
 }
 
+size_t lazy_attn_decode_shared_workspace_size(const lazy_attn_params_t* params, int32_t batch, int32_t max_slots) {
+  if (check_params(params) != LAZY_OK || batch <= 0 || max_slots <= 0) return 0;
+  return (size_t)max_slots * (size_t)batch * params->num_q_heads *
+         ((size_t)params->head_dim * sizeof(uint16_t) + sizeof(float));
+}
+
+int lazy_attn_decode_shared(const lazy_attn_params_t* p, const void* q, const int32_t* q_pos, const void* k_pool,
+                            const void* v_pool, const lazy_shared_item_t* items, int32_t num_items,
+                            const lazy_shared_user_t* users, const int32_t* slot_start, int32_t batch,
+                            int32_t max_slots, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  int e = check_params(p);
+  if (e != LAZY_OK) return e;
+  if (p->num_q_heads / p->num_kv_heads > 16) return LAZY_EUNSUPPORTED;
+  if (batch < 0 || num_items < 0 || max_slots < 0 || (num_items > 0 && max_slots == 0)) return LAZY_EINVAL;
+  if (batch == 0) return LAZY_OK;
+  if (!q || !q_pos || !k_pool || !v_pool || !slot_start || !out || (num_items > 0 && (!items || !users)))
+    return LAZY_EINVAL;
+  if (p->num_kv_heads > 65535) return LAZY_EUNSUPPORTED;
+  const size_t need = lazy_attn_decode_shared_workspace_size(p, batch, max_slots);
+  if (need > 0 && (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 15u))) return LAZY_EWORKSPACE;
+  lazy::SharedArgs a = {};
+  a.q = static_cast<const uint16_t*>(q);
+  a.q_pos = q_pos;
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.items = items;
+  a.users = users;
+  const int64_t rows = (int64_t)batch * p->num_q_heads;
+  a.ws_o = need ? static_cast<uint16_t*>(workspace) : nullptr;
+  a.ws_lse = need ? reinterpret_cast<float*>(static_cast<uint16_t*>(workspace) + (size_t)max_slots * rows * p->head_dim)
+                  : nullptr;
+  a.inv_freq = p->inv_freq;
+  a.batch = batch;
+  a.hq = p->num_q_heads;
+  a.hkv = p->num_kv_heads;
+  a.group = p->num_q_heads / p->num_kv_heads;
+  a.causal = p->causal;
+  a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
+  a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
+  a.scale_log2 = scale_log2(p);
+  return status(lazy::launch_decode_shared(a, num_items, max_slots, slot_start, p->head_dim,
+                                           static_cast<uint16_t*>(out), lse, static_cast<hipStream_t>(stream)));
+}
+
 const char* lazy_attn_strerror(int code) {
   switch (code) {
     case LAZY_OK: return "success";

@@ -37,6 +37,27 @@ struct AttnArgs {
   float scale_log2;           // softmax scale * log2(e)
 };
 
+// Arguments of the chunk-major shared decode kernel.
+struct SharedArgs {
+  const uint16_t* q;                 // [batch][hq][D]
+  const int32_t* q_pos;              // [batch]
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const lazy_shared_item_t* items;   // [num_items]
+  const lazy_shared_user_t* users;
+  uint16_t* ws_o;                    // [max_slots][batch*hq][D] bf16 partial outputs
+  float* ws_lse;                     // [max_slots][batch*hq]
+  const float* inv_freq;             // [D/2] or null
+  int32_t batch;
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;
+  int32_t causal;
+  int32_t local_keys;
+  double rope_log2_base;
+  float scale_log2;
+};
+
 // Packed rows (token, head in group) handled by one prefill workgroup, and keys per decode tile.
 constexpr int kPrefillRowsPerBlock = 128;  // packed rows of a prefill workgroup per row block
 constexpr int kPrefillTileKeys = 64;
@@ -45,6 +66,8 @@ constexpr int kDecodeHeadsPerGroup = 16;
 
 hipError_t launch_prefill(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t stream);
 hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t stream);
+hipError_t launch_decode_shared(const SharedArgs& a, int num_items, int max_slots, const int32_t* slot_start,
+                                int head_dim, uint16_t* out, float* lse, hipStream_t stream);
 hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int splits, int rows, int head_dim,
                           uint16_t* out, float* lse, hipStream_t stream);
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,

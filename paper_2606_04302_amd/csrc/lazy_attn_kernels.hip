@@ -854,6 +854,99 @@ __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, 
   }
 }
 
+// One 32-key tile of one decode wave: V into the wave's LDS slice, K rotated in registers (NoPE store: base row cb
+// of the tile, per-row rows cd0 / cd1 of blocks 0 / 1) and S^T = K Q^T, the key mask, the online-softmax update
+// and O^T += V^T P^T.  lim: this lane's visible keys are the tile keys kk < lim (tile tail and causal rule; it may
+// differ between the lanes' columns).
+template <int D, bool ROT>
+__device__ __forceinline__ void dec_tile(const DecTile<D>& cur, uint16_t* vw, const uint16_t* vlane, const float* cb,
+                                         const float* cd0, const float* cd1, const bf16x8 (&qf)[D / 32],
+                                         f32x4 (&o)[D / 16], float& m2, float& lsum, int lim, float c, int lane) {
+  using S = DecodeSmem<D>;
+  constexpr int SP = DecTile<D>::SP;
+  const int kq = lane >> 4;
+  // V of this tile into the wave's LDS slice (row-major).
+#pragma unroll
+  for (int i = 0; i < DecTile<D>::VC; ++i) {
+    const int cc = lane + 64 * i;
+    *reinterpret_cast<u32x4*>(vw + (cc / (D / 8)) * S::VLD + 8 * (cc % (D / 8))) = cur.v[i];
+  }
+
+  // Rotate K in registers and form S^T = K Q^T, one pair of k-steps (low / high halves) at a time.
+  f32x4 sa[2] = {f32x4{}, f32x4{}};
+#pragma unroll
+  for (int s = 0; s < SP; ++s) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const u32x4 wl = cur.k[b][s][0], wh = cur.k[b][s][1];
+      u32x4 klo, khi;
+      if (ROT) {
+        const float* cdb = b ? cd1 : cd0;
+        float y1[8], y2[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int t = 32 * s + 8 * kq + e;
+          const float x1 = (e & 1) ? bf_hi(wl[e >> 1]) : bf_lo(wl[e >> 1]);
+          const float x2 = (e & 1) ? bf_hi(wh[e >> 1]) : bf_lo(wh[e >> 1]);
+          rotate_pair(x1, x2, *reinterpret_cast<const float2*>(cb + csb_idx<D>(t)),
+                      *reinterpret_cast<const float2*>(cdb + 2 * t), y1[e], y2[e]);
+        }
+        klo = u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])};
+        khi = u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])};
+      } else {
+        klo = wl;
+        khi = wh;
+      }
+      sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(klo), qf[2 * s], sa[b], 0, 0, 0);
+      sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(khi), qf[2 * s + 1], sa[b], 0, 0, 0);
+    }
+  }
+  if (__any(lim < kDecWaveKeys)) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (kappa(b, 4 * kq + i) >= lim) sa[b][i] = -INFINITY;
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sa[b][i]);
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float mt = mx * c;
+  if (__any(mt > m2 + kRescaleSlack)) {
+    const float mnew = fmaxf(m2, mt);
+    const float alpha = m2 == -INFINITY ? 0.f : fast_exp2(m2 - mnew);
+    lsum *= alpha;
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) o[db] *= alpha;
+    m2 = mnew;
+  }
+  const float muse = m2 == -INFINITY ? 0.f : m2;
+  float ps = 0.f;
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float p = fast_exp2(fmaf(sa[b][i], c, -muse));
+      sa[b][i] = p;
+      ps += p;
+    }
+  lsum += ps;
+  const bf16x8 pb = as_bf16x8(u32x4{pack2(sa[0][0], sa[0][1]), pack2(sa[0][2], sa[0][3]),
+                                    pack2(sa[1][0], sa[1][1]), pack2(sa[1][2], sa[1][3])});
+  // O^T += V^T P^T from the wave's V slice (same-wave LDS ordering: written above, read here).
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) {
+    const u32x2 lo = tr_read(vlane + 16 * db);
+    const u32x2 hi = tr_read(vlane + 8 * S::VLD + 16 * db);
+    o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pb, o[db], 0,
+                                                    0, 0);
+  }
+}
+
 template <int D, int KM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_kernel(AttnArgs a) {
   __shared__ DecodeSmem<D> sm;
@@ -989,90 +1082,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
     }
 
-    // V of this tile into the wave's LDS slice (row-major).
-#pragma unroll
-    for (int i = 0; i < DecTile<D>::VC; ++i) {
-      const int cc = lane + 64 * i;
-      *reinterpret_cast<u32x4*>(vw + (cc / (D / 8)) * S::VLD + 8 * (cc % (D / 8))) = cur.v[i];
-    }
-
-    // Rotate K in registers and form S^T = K Q^T, one pair of k-steps (low / high halves) at a time.
-    f32x4 sa[2] = {f32x4{}, f32x4{}};
-    const float* cb = sm.csb[wave][buf];
-#pragma unroll
-    for (int s = 0; s < SP; ++s) {
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const u32x4 wl = cur.k[b][s][0], wh = cur.k[b][s][1];
-        u32x4 klo, khi;
-        if (ROT) {
-          const float* cdb = b ? cd1 : cd0;
-          float y1[8], y2[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int t = 32 * s + 8 * kq + e;
-            const float x1 = (e & 1) ? bf_hi(wl[e >> 1]) : bf_lo(wl[e >> 1]);
-            const float x2 = (e & 1) ? bf_hi(wh[e >> 1]) : bf_lo(wh[e >> 1]);
-            rotate_pair(x1, x2, *reinterpret_cast<const float2*>(cb + csb_idx<D>(t)),
-                        *reinterpret_cast<const float2*>(cdb + 2 * t), y1[e], y2[e]);
-          }
-          klo = u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])};
-          khi = u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])};
-        } else {
-          klo = wl;
-          khi = wh;
-        }
-        sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(klo), qf[2 * s], sa[b], 0, 0, 0);
-        sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(khi), qf[2 * s + 1], sa[b], 0, 0, 0);
-      }
-    }
-    if (nvalid < kDecWaveKeys || (a.causal && b0 + kDecWaveKeys - 1 > qpos)) {
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int kk = kappa(b, 4 * kq + i);
-          const bool ok = kk < nvalid && (!a.causal || b0 + kk <= qpos);
-          if (!ok) sa[b][i] = -INFINITY;
-        }
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sa[b][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mt = mx * c;
-    if (__any(mt > m2 + kRescaleSlack)) {
-      const float mnew = fmaxf(m2, mt);
-      const float alpha = m2 == -INFINITY ? 0.f : fast_exp2(m2 - mnew);
-      lsum *= alpha;
-#pragma unroll
-      for (int db = 0; db < D / 16; ++db) o[db] *= alpha;
-      m2 = mnew;
-    }
-    const float muse = m2 == -INFINITY ? 0.f : m2;
-    float ps = 0.f;
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = fast_exp2(fmaf(sa[b][i], c, -muse));
-        sa[b][i] = p;
-        ps += p;
-      }
-    lsum += ps;
-    const bf16x8 pb = as_bf16x8(u32x4{pack2(sa[0][0], sa[0][1]), pack2(sa[0][2], sa[0][3]),
-                                      pack2(sa[1][0], sa[1][1]), pack2(sa[1][2], sa[1][3])});
-    // O^T += V^T P^T from the wave's V slice (same-wave LDS ordering: written above, read here).
-#pragma unroll
-    for (int db = 0; db < D / 16; ++db) {
-      const u32x2 lo = tr_read(vlane + 16 * db);
-      const u32x2 hi = tr_read(vlane + 8 * S::VLD + 16 * db);
-      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pb, o[db], 0,
-                                                      0, 0);
-    }
+    const int lim = min(nvalid, a.causal ? qpos - b0 + 1 : kDecWaveKeys);
+    dec_tile<D, ROT>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane);
     cur = nxt;
     buf ^= 1;
     have = have_next;
@@ -1127,6 +1138,169 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 }
 
 // ---------------------------------------------------------------------------------------------------------------
+// Chunk-major shared decode: workgroup = (work item, KV head).  A work item is one key range of one stored chunk
+// with up to 16 / G users (requests that hold the chunk, each at its own offset); MFMA column c is the pair
+// (user c / G, query head c % G).  The range's K / V are read once for all users.  Column c's query is rotated by
+// its user's relative offset rel = q_pos - pos_offset, and the keys are used at their local index j (as stored for
+// a local-position store, rotated by R(j) in registers for a NoPE store); key j is visible to the column iff
+// j <= rel under the causal rule.  Waves take the range's 32-key tiles w, w + 4, ... with the next tile in flight,
+// as in decode_kernel, and every (user, item) writes one partial result into its request's slot.
+// ---------------------------------------------------------------------------------------------------------------
+template <int D, int KM>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_shared_kernel(
+    SharedArgs a) {
+  __shared__ DecodeSmem<D> sm;
+  __shared__ float ucs[16][DecodeSmem<D>::CSB];  // per user: cos/sin(rel theta_t) at csb_idx(t)
+  using S = DecodeSmem<D>;
+  constexpr int SP = DecTile<D>::SP;
+  constexpr bool ROT = KM == kKeysNope;
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const cptr<lazy_shared_item_t> item = as_const(a.items) + blockIdx.x;
+  const int g = blockIdx.y;
+  const int64_t koff = item->k_offset, voff = item->v_offset;
+  const int kst = item->k_stride, vst = item->v_stride, kb = item->key_begin, ke = item->key_end;
+  const int u0 = item->user_begin, nu = item->num_users;
+  const int G = a.group;
+  const int col = lane & 15, kq = lane >> 4;
+  const int cu = col / G;
+  const bool cvalid = cu < nu;
+  const int cuser = cvalid ? cu : 0;
+  const lazy_shared_user_t usr = a.users[u0 + cuser];
+  const int rel = a.q_pos[usr.request] - usr.pos_offset;
+
+  // Raw Q of this lane's column and the first tile's K / V before the tables (as in decode_kernel).
+  u32x4 qraw[SP][2];
+  {
+    const uint16_t* qrow = a.q + ((int64_t)usr.request * a.hq + g * G + col % G) * D;
+#pragma unroll
+    for (int s = 0; s < SP; ++s) {
+      const int t0 = 32 * s + 8 * kq;
+      qraw[s][0] = qraw[s][1] = u32x4{0, 0, 0, 0};
+      if (cvalid) {
+        qraw[s][0] = *reinterpret_cast<const u32x4*>(qrow + t0);
+        qraw[s][1] = *reinterpret_cast<const u32x4*>(qrow + D / 2 + t0);
+      }
+    }
+  }
+  const uint16_t* kbase = a.k_pool + koff + (int64_t)g * kst * D;
+  const uint16_t* vbase = a.v_pool + voff + (int64_t)g * vst * D;
+  const int ntiles = (ke - kb + kDecWaveKeys - 1) / kDecWaveKeys;
+  int tile = wave;
+  DecTile<D> cur, nxt;
+  if (tile < ntiles) {
+    const int j0 = kb + kDecWaveKeys * tile;
+    dec_fetch<D>(cur, kbase + (int64_t)j0 * D, vbase + (int64_t)j0 * D, min(kDecWaveKeys, ke - j0), lane);
+  }
+
+  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
+  __syncthreads();
+  if (ROT) {
+    for (int e = tid; e < kDecWaveKeys * (D / 2); e += kThreads) {
+      const int dr = e / (D / 2), t = e % (D / 2);
+      *reinterpret_cast<float2*>(sm.csd + dr * S::CSD_LD + 2 * t) = rope_cs(dr, sm.freq[t]);
+    }
+    if (tile < ntiles && lane < D / 2)
+      *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) =
+          rope_cs(kb + kDecWaveKeys * tile, sm.freq[lane]);
+  }
+  for (int e = tid; e < nu * (D / 2); e += kThreads) {
+    const int u = e / (D / 2), t = e % (D / 2);
+    const lazy_shared_user_t uu = a.users[u0 + u];
+    *reinterpret_cast<float2*>(&ucs[u][csb_idx<D>(t)]) = rope_cs(a.q_pos[uu.request] - uu.pos_offset, sm.freq[t]);
+  }
+  __syncthreads();
+
+  // Q fragments: R(rel) q for this lane's column.
+  bf16x8 qf[D / 32];
+#pragma unroll
+  for (int s = 0; s < SP; ++s) {
+    float y1[8], y2[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float x1 = (e & 1) ? bf_hi(qraw[s][0][e >> 1]) : bf_lo(qraw[s][0][e >> 1]);
+      const float x2 = (e & 1) ? bf_hi(qraw[s][1][e >> 1]) : bf_lo(qraw[s][1][e >> 1]);
+      rotate_by(x1, x2, *reinterpret_cast<const float2*>(&ucs[cuser][csb_idx<D>(32 * s + 8 * kq + e)]), y1[e],
+                y2[e]);
+    }
+    qf[2 * s] = as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])});
+    qf[2 * s + 1] =
+        as_bf16x8(u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])});
+  }
+
+  f32x4 o[D / 16];
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) o[db] = f32x4{};
+  float m2 = -INFINITY, lsum = 0.f;
+  const float c = a.scale_log2;
+  uint16_t* vw = sm.v[wave];
+  const uint16_t* vlane = vw + (16 * (kq >> 1) + 4 * (kq & 1) + ((lane & 15) >> 2)) * S::VLD + 4 * (lane & 3);
+  const float* cd0 = sm.csd + kappa(0, col) * S::CSD_LD;
+  const float* cd1 = sm.csd + kappa(1, col) * S::CSD_LD;
+  int buf = 0;
+  while (tile < ntiles) {
+    const int j0 = kb + kDecWaveKeys * tile;
+    const int nvalid = min(kDecWaveKeys, ke - j0);
+    const int next = tile + 4;
+    if (next < ntiles) {
+      const int j1 = kb + kDecWaveKeys * next;
+      dec_fetch<D>(nxt, kbase + (int64_t)j1 * D, vbase + (int64_t)j1 * D, min(kDecWaveKeys, ke - j1), lane);
+      if (ROT && lane < D / 2)
+        *reinterpret_cast<float2*>(sm.csb[wave][buf ^ 1] + csb_idx<D>(lane)) = rope_cs(j1, sm.freq[lane]);
+    }
+    const int lim = min(nvalid, a.causal ? rel - j0 + 1 : kDecWaveKeys);
+    dec_tile<D, ROT>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane);
+    cur = nxt;
+    buf ^= 1;
+    tile = next;
+  }
+
+  // Merge the four waves' states through LDS, then one partial result per (user, query head).
+  float ltot = lsum + __shfl_xor(lsum, 16);
+  ltot += __shfl_xor(ltot, 32);
+  __syncthreads();
+  float* macc = reinterpret_cast<float*>(sm.v[0]);  // [4][D][16]
+  float* mm = macc + 4 * D * 16;                    // [4][16]
+  float* ml = mm + 4 * 16;                          // [4][16]
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) macc[(wave * D + 16 * db + 4 * kq + i) * 16 + col] = o[db][i];
+  if (kq == 0) {
+    mm[wave * 16 + col] = m2;
+    ml[wave * 16 + col] = ltot;
+  }
+  __syncthreads();
+  const int64_t rows = (int64_t)a.batch * a.hq;
+  for (int idx = tid; idx < 16 * (D / 4); idx += kThreads) {
+    const int hc = idx & 15, d4 = idx >> 4;
+    if (hc / G >= nu) continue;
+    float mw[4], mmax = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      mw[w] = mm[w * 16 + hc];
+      mmax = fmaxf(mmax, mw[w]);
+    }
+    float l = 0.f;
+    f32x4 acc = f32x4{};
+    if (mmax != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float sc = fast_exp2(mw[w] - mmax);
+        l = fmaf(ml[w * 16 + hc], sc, l);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] = fmaf(macc[(w * D + 4 * d4 + e) * 16 + hc], sc, acc[e]);
+      }
+    }
+    const lazy_shared_user_t uu = a.users[u0 + hc / G];
+    const int64_t wrow = (int64_t)uu.slot * rows + (int64_t)uu.request * a.hq + g * G + hc % G;
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    *reinterpret_cast<u32x2*>(a.ws_o + wrow * D + 4 * d4) =
+        u32x2{pack2(acc[0] * inv, acc[1] * inv), pack2(acc[2] * inv, acc[3] * inv)};
+    if (d4 == 0) a.ws_lse[wrow] = l > 0.f ? (mmax + log2f(l)) * kLn2 : -INFINITY;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
 // Split-KV merge: per row, the splits' normalised outputs weighted by exp(lse_s - max lse), divided by the sum of
 // the weights.  A row is served by kCombineGroups x D / 8 lanes of one wave: lane (g, d8) loads 8 dims (16 bytes)
 // of the splits g, g + kCombineGroups, ...; the groups' partial sums are then added across lanes.  Every thread
@@ -1138,6 +1312,7 @@ constexpr int kCombineGroups = 4;
 template <int D>
 __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __restrict__ part_o,
                                                            const float* __restrict__ part_lse, int splits, int rows,
+                                                           const int32_t* __restrict__ slot_start, int hq,
                                                            uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int TPR = D / 8;
   constexpr int LPR = TPR * kCombineGroups;  // lanes per row: 64 (D = 128) or 32 (D = 64)
@@ -1147,6 +1322,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __res
   const int grp = (threadIdx.x / TPR) % kCombineGroups;
   // Rows past the end take part in the shuffles with no memory access (the whole wave stays converged).
   const bool live = row < rows;
+  // With slot_start (shared decode), row r * hq + h of request r merges that request's own slot count.
+  if (live && slot_start) splits = slot_start[row / hq + 1] - slot_start[row / hq];
   float mmax = -INFINITY;
   if (live) {
     for (int s0 = 0; s0 < splits; s0 += 8) {
@@ -1320,9 +1497,11 @@ hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int spl
   const int per_block = kThreads / (head_dim / 8 * kCombineGroups);
   const dim3 grid((rows + per_block - 1) / per_block);
   if (head_dim == 128)
-    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, out, lse);
+    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, nullptr, 1,
+                       out, lse);
   else
-    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, out, lse);
+    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, nullptr, 1,
+                       out, lse);
   return hipGetLastError();
 }
 
@@ -1338,6 +1517,37 @@ hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStre
   const hipError_t e = head_dim == 128 ? decode_dk<128>(a, km, st) : decode_dk<64>(a, km, st);
   if (e != hipSuccess || a.splits == 1) return e;
   return launch_combine(a.ws_o, a.ws_lse, a.splits, a.total_q * a.hq, head_dim, a.out, a.lse, st);
+}
+
+hipError_t launch_decode_shared(const SharedArgs& a, int num_items, int max_slots, const int32_t* slot_start,
+                                int head_dim, uint16_t* out, float* lse, hipStream_t st) {
+  const int rows = a.batch * a.hq;
+  if (num_items > 0) {
+    const dim3 grid(num_items, a.hkv);
+    if (head_dim == 128) {
+      if (a.local_keys)
+        hipLaunchKernelGGL((decode_shared_kernel<128, kKeysLocal>), grid, dim3(kThreads), 0, st, a);
+      else
+        hipLaunchKernelGGL((decode_shared_kernel<128, kKeysNope>), grid, dim3(kThreads), 0, st, a);
+    } else {
+      if (a.local_keys)
+        hipLaunchKernelGGL((decode_shared_kernel<64, kKeysLocal>), grid, dim3(kThreads), 0, st, a);
+      else
+        hipLaunchKernelGGL((decode_shared_kernel<64, kKeysNope>), grid, dim3(kThreads), 0, st, a);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  // Ragged merge of every request's slots (a request without slots gets out = 0, lse = -inf).
+  const int per_block = kThreads / (head_dim / 8 * kCombineGroups);
+  const dim3 grid((rows + per_block - 1) / per_block);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kThreads), 0, st, a.ws_o, a.ws_lse, max_slots, rows,
+                       slot_start, a.hq, out, lse);
+  else
+    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(kThreads), 0, st, a.ws_o, a.ws_lse, max_slots, rows,
+                       slot_start, a.hq, out, lse);
+  return hipGetLastError();
 }
 
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,

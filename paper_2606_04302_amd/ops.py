@@ -43,6 +43,12 @@ class LazyChunk(ctypes.Structure):
 
 assert ctypes.sizeof(LazyChunk) == CHUNK_DTYPE.itemsize == 32
 
+# Plan records of the chunk-major shared decode (lazy_shared_item_t, lazy_shared_user_t).
+ITEM_DTYPE = np.dtype([("k_offset", "<i8"), ("v_offset", "<i8"), ("k_stride", "<i4"), ("v_stride", "<i4"),
+                       ("key_begin", "<i4"), ("key_end", "<i4"), ("user_begin", "<i4"), ("num_users", "<i4")])
+USER_DTYPE = np.dtype([("request", "<i4"), ("pos_offset", "<i4"), ("slot", "<i4"), ("reserved", "<i4")])
+assert ITEM_DTYPE.itemsize == 40 and USER_DTYPE.itemsize == 16
+
 _ATTN_PREFILL = [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_i32, _c_i32,
                  _c_i32, _c_p, _c_p, _c_p, _c_sz, _c_p]
 _ATTN_DECODE = [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_i32, _c_p, _c_p,
@@ -59,6 +65,11 @@ SIGNATURES = {
                                     _c_p]),
     "lazy_attn_validate": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64,
                                     ctypes.POINTER(_c_i64), ctypes.POINTER(ctypes.c_char_p)]),
+    "lazy_shared_decode_plan": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_i32, _c_i32, _c_p, _c_i32,
+                                         _c_p, _c_i32, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32), _c_p]),
+    "lazy_attn_decode_shared": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_p,
+                                         _c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_sz, _c_p]),
+    "lazy_attn_decode_shared_workspace_size": (_c_sz, [ctypes.POINTER(LazyAttnParams), _c_i32, _c_i32]),
     "lazy_attn_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "lazy_attn_version": (ctypes.c_int, []),
 }
@@ -289,6 +300,94 @@ def validate(cfg: Config, q_start, q_pos0, chunks: np.ndarray, chunk_start, k_po
                                     cs.ctypes.data, cs.size - 1, k_pool_elems, v_pool_elems, ctypes.byref(bad),
                                     ctypes.byref(why))
     return code, int(bad.value), (why.value or b"").decode()
+
+
+@dataclass
+class SharedPlan:
+    """A chunk-major shared-decode plan (host arrays from lazy_shared_decode_plan)."""
+
+    items: np.ndarray       # ITEM_DTYPE
+    users: np.ndarray       # USER_DTYPE
+    slot_start: np.ndarray  # int32 [batch+1]
+
+    @property
+    def max_slots(self) -> int:
+        return int(np.diff(self.slot_start).max()) if self.slot_start.size > 1 else 0
+
+
+def shared_decode_plan(cfg: Config, chunks: np.ndarray, chunk_start, max_keys_per_item: int = 0) -> SharedPlan:
+    """lazy_shared_decode_plan on host tables (grows the output arrays if the first guess is too small)."""
+    chunks = np.ascontiguousarray(chunks, dtype=CHUNK_DTYPE)
+    cs = np.ascontiguousarray(chunk_start, dtype=np.int32)
+    batch = cs.size - 1
+    step = max_keys_per_item or 1024
+    cap = max(1, int(np.sum((chunks["len"].astype(np.int64) + step - 1) // step)) if chunks.size else 1)
+    p = cfg.c()
+    n_items, n_users = _c_i32(0), _c_i32(0)
+    slot_start = np.zeros(batch + 1, dtype=np.int32)
+    for _ in range(2):
+        items = np.zeros(cap, dtype=ITEM_DTYPE)
+        users = np.zeros(cap, dtype=USER_DTYPE)
+        code = lib().lazy_shared_decode_plan(ctypes.byref(p), chunks.ctypes.data if chunks.size else None,
+                                             cs.ctypes.data, batch, max_keys_per_item, items.ctypes.data, cap,
+                                             users.ctypes.data, cap, ctypes.byref(n_items), ctypes.byref(n_users),
+                                             slot_start.ctypes.data)
+        if code == LAZY_EINVAL and max(n_items.value, n_users.value) > cap:
+            cap = max(n_items.value, n_users.value)
+            continue
+        _check(code, "lazy_shared_decode_plan")
+        return SharedPlan(items[: n_items.value].copy(), users[: n_users.value].copy(), slot_start)
+    raise RuntimeError("lazy_shared_decode_plan: capacity did not converge")
+
+
+@dataclass
+class DevicePlan:
+    items: torch.Tensor
+    users: torch.Tensor
+    slot_start: torch.Tensor
+    num_items: int
+    max_slots: int
+
+
+def upload_plan(plan: SharedPlan, device="cuda") -> DevicePlan:
+    def raw(a):
+        b = np.ascontiguousarray(a).view(np.uint8).reshape(-1)
+        return torch.from_numpy(b.copy() if b.size else np.zeros(16, np.uint8)).to(device)
+    return DevicePlan(raw(plan.items), raw(plan.users), torch.from_numpy(plan.slot_start.copy()).to(device),
+                      int(plan.items.size), plan.max_slots)
+
+
+def decode_shared_workspace_size(cfg: Config, batch: int, max_slots: int) -> int:
+    p = cfg.c()
+    return int(lib().lazy_attn_decode_shared_workspace_size(ctypes.byref(p), batch, max_slots))
+
+
+def decode_shared(cfg: Config, q, q_pos, k_pool, v_pool, plan: DevicePlan, out=None, lse=None, workspace=None,
+                  stream=None):
+    """lazy_attn_decode_shared over an uploaded plan.  q is [B, Hq, D].  Returns (out, lse)."""
+    _dev(q, torch.bfloat16, "q")
+    _dev(k_pool, torch.bfloat16, "k_pool")
+    _dev(v_pool, torch.bfloat16, "v_pool")
+    _dev(q_pos, torch.int32, "q_pos")
+    _dev(plan.slot_start, torch.int32, "slot_start")
+    _need(q.dim() == 3 and q.shape[1] == cfg.num_q_heads and q.shape[2] == cfg.head_dim, "q must be [B, Hq, D]")
+    batch = q.shape[0]
+    _need(q_pos.numel() == batch and plan.slot_start.numel() == batch + 1, "table sizes disagree with the batch")
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, torch.bfloat16, "out")
+    if lse is not None:
+        _dev(lse, torch.float32, "lse")
+        _need(lse.shape == (batch, cfg.num_q_heads), "lse must be [B, Hq]")
+    nbytes = decode_shared_workspace_size(cfg, batch, plan.max_slots)
+    workspace = _workspace(nbytes, q.device, workspace)
+    p = cfg.c()
+    _check(lib().lazy_attn_decode_shared(ctypes.byref(p), q.data_ptr(), q_pos.data_ptr(), k_pool.data_ptr(),
+                                         v_pool.data_ptr(), plan.items.data_ptr(), plan.num_items,
+                                         plan.users.data_ptr(), plan.slot_start.data_ptr(), batch, plan.max_slots,
+                                         out.data_ptr(), _ptr(lse), _ptr(workspace), nbytes, _stream(stream)),
+           "lazy_attn_decode_shared")
+    return out, lse
 
 
 # ---------------------------------------------------------------------------------------------------------------

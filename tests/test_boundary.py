@@ -237,3 +237,156 @@ int main() {
     res = subprocess.run([str(exe)], capture_output=True, text=True)
     assert res.returncode == 0, res.stdout + res.stderr
     assert "ok=1" in res.stdout
+
+
+# ---------------------------------------------------------------------------------------------------------------
+# Chunk-major shared decode: the host planner (CPU) and the plan record layouts.
+# ---------------------------------------------------------------------------------------------------------------
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="gcc missing")
+def test_shared_plan_layout_matches_header(tmp_path, ops):
+    src = tmp_path / "plan_layout.c"
+    src.write_text(
+        '#include <stdio.h>\n#include <stddef.h>\n#include "lazy_attn.h"\n'
+        "int main(void){"
+        'printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(lazy_shared_item_t),'
+        " offsetof(lazy_shared_item_t, v_offset), offsetof(lazy_shared_item_t, k_stride),"
+        " offsetof(lazy_shared_item_t, v_stride), offsetof(lazy_shared_item_t, key_begin),"
+        " offsetof(lazy_shared_item_t, key_end), offsetof(lazy_shared_item_t, user_begin),"
+        " offsetof(lazy_shared_item_t, num_users), sizeof(lazy_shared_user_t));"
+        'printf("%zu %zu %zu\\n", offsetof(lazy_shared_user_t, pos_offset), offsetof(lazy_shared_user_t, slot),'
+        " offsetof(lazy_shared_user_t, reserved));"
+        "return 0;}"
+    )
+    exe = tmp_path / "plan_layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    a, b = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")[:2]
+    it = ops.ITEM_DTYPE
+    us = ops.USER_DTYPE
+    assert [int(x) for x in a.split()] == [it.itemsize] + [it.fields[n][1] for n in (
+        "v_offset", "k_stride", "v_stride", "key_begin", "key_end", "user_begin", "num_users")] + [us.itemsize]
+    assert [int(x) for x in b.split()] == [us.fields[n][1] for n in ("pos_offset", "slot", "reserved")]
+
+
+def _check_plan(w, plan, g, step):
+    """Invariants of a plan: every piece of every record is exactly one (user, item) pair with the record's stored
+    range, offset and request; slots of a request are 0.. in table order; items respect the column budget and are
+    sorted by key count."""
+    per_item = 16 // g
+    seen = {}
+    for it in plan.items:
+        assert 1 <= it["num_users"] <= per_item
+        assert 0 <= it["key_begin"] < it["key_end"] and it["key_end"] - it["key_begin"] <= step
+        for u in plan.users[it["user_begin"]: it["user_begin"] + it["num_users"]]:
+            key = (int(u["request"]), int(u["slot"]))
+            assert key not in seen
+            seen[key] = (int(it["k_offset"]), int(it["v_offset"]), int(it["k_stride"]), int(it["v_stride"]),
+                         int(it["key_begin"]), int(it["key_end"]), int(u["pos_offset"]))
+    lens = plan.items["key_end"] - plan.items["key_begin"]
+    assert np.all(np.diff(lens) <= 0)
+    expect = {}
+    for r in range(w.batch):
+        slot = 0
+        for rec in w.chunks[w.chunk_start[r]: w.chunk_start[r + 1]]:
+            for kb in range(0, int(rec["len"]), step):
+                expect[(r, slot)] = (int(rec["k_offset"]), int(rec["v_offset"]), int(rec["k_stride"]),
+                                     int(rec["v_stride"]), kb, min(int(rec["len"]), kb + step), int(rec["pos_offset"]))
+                slot += 1
+        assert plan.slot_start[r + 1] - plan.slot_start[r] == slot
+    assert seen == expect
+    assert plan.slot_start[0] == 0
+
+
+@pytest.mark.parametrize("step", [0, 100, 1000])
+def test_shared_plan_covers_every_record_piece_once(ops, step):
+    w = W.rag_decode(seed=5, batch=9, hq=8, hkv=2, n_chunks=5, chunk_len=300, pool_chunks=7, tail_len=9,
+                     tail_cap=16)
+    plan = ops.shared_decode_plan(ops.config_of(w), w.chunks, w.chunk_start, step)
+    _check_plan(w, plan, 4, step or 1024)
+    # sharing: the 9 requests x 5 chunks read only 7 stored chunks, so there are far fewer items than records
+    if step == 0:
+        assert plan.items.size <= 7 * 3 + 9 and plan.users.size == len(w.chunks)
+
+
+def test_shared_plan_g7_and_zipf_reuse(ops):
+    w = W.varlen_rag(seed=6, batch=6, hq=28, hkv=4, pool_chunks=12, len_lo=10, len_hi=400, k_lo=3, k_hi=6,
+                     q_lo=1, q_hi=1)
+    plan = ops.shared_decode_plan(ops.config_of(w), w.chunks, w.chunk_start, 128)
+    _check_plan(w, plan, 7, 128)
+
+
+def test_shared_plan_errors(ops):
+    w = W.rag_decode(seed=7, batch=2, hq=8, hkv=2, n_chunks=2, chunk_len=40, pool_chunks=3, tail_len=2, tail_cap=4)
+    L = ops.lib()
+    p = ops.config_of(w).c()
+    ch = np.ascontiguousarray(w.chunks)
+    cs = np.ascontiguousarray(w.chunk_start, dtype=np.int32)
+    items = np.zeros(1, dtype=ops.ITEM_DTYPE)
+    users = np.zeros(1, dtype=ops.USER_DTYPE)
+    ni, nu = ctypes.c_int32(0), ctypes.c_int32(0)
+    ss = np.zeros(3, dtype=np.int32)
+    code = L.lazy_shared_decode_plan(ctypes.byref(p), ch.ctypes.data, cs.ctypes.data, 2, 0, items.ctypes.data, 1,
+                                     users.ctypes.data, 1, ctypes.byref(ni), ctypes.byref(nu), ss.ctypes.data)
+    assert code == ops.LAZY_EINVAL and ni.value > 1 and nu.value == len(w.chunks)  # capacity: counts still reported
+    big = ops.Config(34, 2, 128, 1e4)  # G = 17 columns do not fit one workgroup
+    pb = big.c()
+    assert L.lazy_shared_decode_plan(ctypes.byref(pb), ch.ctypes.data, cs.ctypes.data, 2, 0, None, 0, None, 0,
+                                     ctypes.byref(ni), ctypes.byref(nu), ss.ctypes.data) == ops.LAZY_EUNSUPPORTED
+    bad = ch.copy()
+    bad["len"][1] = -3
+    assert L.lazy_shared_decode_plan(ctypes.byref(p), bad.ctypes.data, cs.ctypes.data, 2, 0, None, 0, None, 0,
+                                     ctypes.byref(ni), ctypes.byref(nu), ss.ctypes.data) == ops.LAZY_EDATA
+    assert L.lazy_shared_decode_plan(ctypes.byref(p), ch.ctypes.data, cs.ctypes.data, 2, -1, None, 0, None, 0,
+                                     ctypes.byref(ni), ctypes.byref(nu), ss.ctypes.data) == ops.LAZY_EINVAL
+    # scalar checks of the device entry point (no launch)
+    assert L.lazy_attn_decode_shared(ctypes.byref(pb), 1, 1, 1, 1, 1, 1, 1, 1, 2, 1, 1, None, None, 0,
+                                     None) == ops.LAZY_EUNSUPPORTED
+    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, 1, 1, 2, 0, 1, None, None, 0,
+                                     None) == ops.LAZY_EINVAL
+    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, 1, 1, 2, 4, 1, None, None, 0,
+                                     None) == ops.LAZY_EWORKSPACE
+    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, 1, 1, 0, 4, 1, None, None, 0,
+                                     None) == ops.LAZY_OK
+    assert ops.decode_shared_workspace_size(ops.config_of(w), 2, 5) == 5 * 2 * 8 * (2 * 128 + 4)
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ missing")
+def test_shared_plan_under_address_and_ub_sanitizers(tmp_path):
+    drv = tmp_path / "plan_drv.cpp"
+    drv.write_text(r'''
+#include <stdio.h>
+#include <vector>
+#include "lazy_attn.h"
+int main() {
+  lazy_attn_params_t p = {8, 2, 128, 1, 1e4f, 0.f, nullptr, 0, 0};
+  // 3 requests; records 0/2/4 read the same stored chunk at different offsets, one 2500-key private record
+  std::vector<lazy_chunk_t> c = {{0, 4096, 300, 0, 300, 300}, {9000, 9500, 20, 300, 32, 32},
+                                 {0, 4096, 300, 50, 300, 300}, {20000, 90000, 2500, 0, 2500, 2500},
+                                 {0, 4096, 300, 7, 300, 300}};
+  int32_t cs[4] = {0, 2, 4, 5};
+  int fails = 0;
+  for (int step : {0, 1, 64, 1000}) {
+    int32_t ni = 0, nu = 0, ss[4];
+    int code = lazy_shared_decode_plan(&p, c.data(), cs, 3, step, nullptr, 0, nullptr, 0, &ni, &nu, ss);
+    if (code != LAZY_EINVAL || ni <= 0 || nu <= 0) ++fails;
+    std::vector<lazy_shared_item_t> items(ni);
+    std::vector<lazy_shared_user_t> users(nu);
+    code = lazy_shared_decode_plan(&p, c.data(), cs, 3, step, items.data(), ni, users.data(), nu, &ni, &nu, ss);
+    if (code != LAZY_OK || ss[0] != 0 || ss[3] != nu) ++fails;
+    for (const auto& it : items)
+      if (it.user_begin < 0 || it.user_begin + it.num_users > nu || it.num_users < 1 || it.num_users > 4) ++fails;
+  }
+  int32_t ni = 0, nu = 0, ss[4];
+  if (lazy_shared_decode_plan(&p, nullptr, cs, 3, 0, nullptr, 0, nullptr, 0, &ni, &nu, ss) != LAZY_EINVAL) ++fails;
+  int32_t empty[1] = {0};
+  if (lazy_shared_decode_plan(&p, nullptr, empty, 0, 0, nullptr, 0, nullptr, 0, &ni, &nu, ss) != LAZY_OK) ++fails;
+  printf("sanitized planner ok=%d\n", fails == 0);
+  return fails;
+}
+''')
+    exe = tmp_path / "plan_drv"
+    subprocess.run(["g++", "-std=c++17", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-I",
+                    os.path.join(ROOT, "include"), str(drv), os.path.join(B.CSRC, "lazy_attn_plan.cpp"), "-o",
+                    str(exe)], check=True)
+    res = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert "ok=1" in res.stdout

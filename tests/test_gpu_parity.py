@@ -382,3 +382,75 @@ def test_local_key_store_position_discrimination():
                 w2.chunks["pos_offset"][i] += d
                 e1 = np.abs(o[rows] - oracle(w2, key_positions="local")[0][rows]).mean()
                 assert e1 > 8 * e0, (kind, i, d, e0, e1)
+
+
+# --------------------------------------------------------------------------------------------------------------
+# Chunk-major shared decode: a host plan groups records that read the same stored keys; every group's keys are read
+# once for all of its users.  Same results as the per-request decode (the oracle decides).
+def run_shared_and_check(w, tag, cfg_kw=None, step=0):
+    cfg = ops.config_of(w, **(cfg_kw or {}))
+    plan = ops.shared_decode_plan(cfg, w.chunks, w.chunk_start, step)
+    dw = ops.upload(w)
+    dp = ops.upload_plan(plan)
+    lse = torch.empty((w.batch, w.num_q_heads), dtype=torch.float32, device="cuda")
+    out, _ = ops.decode_shared(cfg, dw.q, dw.q_pos0, dw.pool, dw.pool, dp, lse=lse)
+    torch.cuda.synchronize()
+    okw = {"key_positions": "local"} if (cfg_kw or {}).get("key_positions") == ops.KEYS_LOCAL else {}
+    ref_o, ref_l = oracle(w, **okw)
+    print(f"{tag}: {plan.items.size} items for {len(w.chunks)} records, max slots {plan.max_slots}", flush=True)
+    assert_close(out, lse, ref_o, ref_l, tag=tag)
+    return plan
+
+
+SHARED_CASES = {
+    # name: (rag_decode kwargs, cfg kwargs, max keys per item)
+    "g4_shared": (dict(seed=101, batch=6, hq=8, hkv=2, d=128, n_chunks=4, chunk_len=300, pool_chunks=5, tail_len=9,
+                       tail_cap=16), {}, 0),
+    "g4_shared_split100": (dict(seed=102, batch=6, hq=8, hkv=2, d=128, n_chunks=4, chunk_len=300, pool_chunks=5,
+                                tail_len=9, tail_cap=16), {}, 100),
+    "g7_d64_split37": (dict(seed=103, batch=5, hq=14, hkv=2, d=64, n_chunks=3, chunk_len=150, pool_chunks=4,
+                            tail_len=33, tail_cap=40), {}, 37),
+    "mha_g1": (dict(seed=104, batch=20, hq=4, hkv=4, d=128, n_chunks=2, chunk_len=257, pool_chunks=3, tail_len=2,
+                    tail_cap=2), {}, 0),
+    "g16_one_user_per_item": (dict(seed=105, batch=3, hq=32, hkv=2, d=128, n_chunks=2, chunk_len=90,
+                                   pool_chunks=2, tail_len=5, tail_cap=8), {}, 64),
+}
+
+
+@pytest.mark.parametrize("local", [False, True])
+@pytest.mark.parametrize("name", list(SHARED_CASES))
+def test_shared_decode_matches_oracle(name, local):
+    kw, ckw, step = SHARED_CASES[name]
+    ckw = {**ckw, **(LOCAL if local else {})}
+    plan = run_shared_and_check(W.rag_decode(**kw), f"shared {name} {'local' if local else 'nope'}", ckw, step)
+    if name == "g4_shared":
+        assert plan.items.size < sum(1 for _ in W.rag_decode(**kw).chunks)  # chunks really are shared
+
+
+def test_shared_decode_edge_cases():
+    """A request without records (out = 0, lse = -inf), one whose only chunk lies after the query (causal: nothing
+    visible), records shorter than a tile, the same chunk twice in one request at different offsets, non-causal."""
+    reqs = [
+        dict(chunks=[("a", 70, 0), ("b", 5, 70), ("a", 70, 200)], q_len=1, q_pos0=300),
+        dict(chunks=[], q_len=1, q_pos0=10),
+        dict(chunks=[("b", 5, 50)], q_len=1, q_pos0=20),
+        dict(chunks=[("a", 70, 1000), (1, 1070), ("b", 5, 5)], q_len=1, q_pos0=1070),
+    ]
+    w = W.custom(106, 8, 2, 128, 1e4, reqs, kind="decode", slack_fill=np.nan)
+    for local in (False, True):
+        run_shared_and_check(w, f"shared edge {local}", LOCAL if local else {})
+    w.causal = False
+    run_shared_and_check(w, "shared edge non-causal")
+
+
+def test_shared_decode_full_size_sampled():
+    """The benchmark's decode batch (64 requests, chunks shared ~4x) through the shared path, sampled requests."""
+    w = W.rag_decode(seed=2)
+    cfg = ops.config_of(w)
+    plan = ops.shared_decode_plan(cfg, w.chunks, w.chunk_start)
+    dw = ops.upload(w)
+    out, _ = ops.decode_shared(cfg, dw.q, dw.q_pos0, dw.pool, dw.pool, ops.upload_plan(plan))
+    torch.cuda.synchronize()
+    ref_o, ref_l = oracle(w, requests=[0, 31, 63])
+    rows = rows_of(w, [0, 31, 63])
+    assert_close(out, None, ref_o, ref_l, rows, tag="shared full rag_decode")
