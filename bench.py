@@ -198,6 +198,18 @@ def other_configs(dev, steps: int, warmup: int, log):
     log("icl: timing 128 decode steps")
     dec_ms = timed(decode_all, reps, 2)
 
+    # Chunk-major shared decode steps: the exemplar pool is read once per step for the four requests.
+    plans = [ops.upload_plan(ops.shared_decode_plan(cfg, ch, w.chunk_start), dev) for ch, _, _ in tables]
+    wsh = torch.empty(max(16, max(ops.decode_shared_workspace_size(cfg, w.batch, pl.max_slots) for pl in plans)),
+                      dtype=torch.uint8, device=dev)
+
+    def decode_shared_all():
+        for s, (_, _, qp) in enumerate(tables):
+            ops.decode_shared(cfg, qd, qp, dw.pool, dw.pool, plans[s], out=outd, workspace=wsh)
+
+    log("icl: timing 128 shared decode steps")
+    shared_ms = timed(decode_shared_all, reps, 2)
+
     # Baseline: keys materialised once at their final lengths; per-step tables point into the copy.
     final = tables[-1][0]
     mat_fn, k_mat, ch_mat = materialized(w, dw, final)
@@ -233,13 +245,17 @@ def other_configs(dev, steps: int, warmup: int, log):
         "decode_logical_hbm_gbps": round(dec_bytes / (dec_ms * 1e-3) / 1e9, 1),
         "decode_logical_hbm_frac": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
         "decode_logical_gb": round(dec_bytes / 1e9, 3),
+        "shared_decode_128_steps_ms": round(shared_ms, 4),
+        "shared_decode_logical_gbps": round(dec_bytes / (shared_ms * 1e-3) / 1e9, 1),
         "unique_kv_mb": round(A.unique_kv_bytes(w) / 1e6, 1),
         "lazy_prefill_plus_decode_ms": round(lazy_total, 4),
+        "lazy_prefill_plus_shared_decode_ms": round(pre_ms + shared_ms, 4),
         "materialize_ms": round(mat_ms, 5),
         "plain_prefill_ms": round(plain_pre_ms, 5),
         "plain_decode_128_steps_ms": round(plain_dec_ms, 4),
         "materialize_then_attend_ms": round(base_total, 4),
         "speedup_vs_materialize": round(base_total / lazy_total, 3),
+        "speedup_vs_materialize_shared_decode": round(base_total / (pre_ms + shared_ms), 3),
     }
     del k_mat, dw, ws, wsd
 
@@ -440,6 +456,19 @@ def main() -> int:
         cfgd_local = ops.config_of(wd, key_positions=ops.KEYS_LOCAL)
         dlocal = timed(lambda: ops.decode(cfgd_local, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
                                           wd.max_kv_len, out=outd, lse=lsed, workspace=wsd), args.steps, args.warmup)
+        # Chunk-major shared decode of the same batch: every stored chunk is read once for all of its users.
+        t0 = time.perf_counter()
+        plan = ops.shared_decode_plan(cfgd, wd.chunks, wd.chunk_start)
+        plan_ms = (time.perf_counter() - t0) * 1e3
+        dplan = ops.upload_plan(plan, dev)
+        wss = torch.empty(max(16, ops.decode_shared_workspace_size(cfgd, wd.batch, plan.max_slots)),
+                          dtype=torch.uint8, device=dev)
+        dshared = timed(lambda: ops.decode_shared(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dplan, out=outd,
+                                                  lse=lsed, workspace=wss), args.steps, args.warmup)
+        dshared_local = timed(lambda: ops.decode_shared(cfgd_local, dd.q, dd.q_pos0, dd.pool, dd.pool, dplan,
+                                                        out=outd, lse=lsed, workspace=wss), args.steps, args.warmup)
+        item_keys = (plan.items["key_end"] - plan.items["key_begin"]).astype(np.int64)
+        shared_read_mb = float(item_keys.sum()) * wd.num_kv_heads * wd.head_dim * 2 * 2 / 1e6
         tkv = int(wd.chunks["len"].astype(np.int64).sum())
         kmd = torch.empty(cfgd.num_kv_heads * tkv * cfgd.head_dim, dtype=torch.bfloat16, device=dev)
         chd = torch.empty_like(dd.chunks)
@@ -462,6 +491,13 @@ def main() -> int:
             "rotation_overhead": round(dms / dnorot - 1.0, 4),
             "local_keys_ms": round(dlocal, 5),
             "local_keys_logical_hbm_gbps": round(dbytes / (dlocal * 1e-3) / 1e9, 1),
+            "shared_ms": round(dshared, 5),
+            "shared_logical_gbps": round(dbytes / (dshared * 1e-3) / 1e9, 1),
+            "shared_local_keys_ms": round(dshared_local, 5),
+            "shared_kv_read_mb": round(shared_read_mb, 1),
+            "shared_items": int(plan.items.size),
+            "shared_plan_host_ms": round(plan_ms, 3),
+            "shared_speedup_vs_per_request": round(dms / dshared, 3),
             "materialize_ms": round(dmat, 5),
             "plain_decode_ms": round(dplain, 5),
             "materialize_then_attend_ms": round(dmat + dplain, 5),

@@ -648,7 +648,8 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
       }
     }
   }
-  PLoader<D, KM, NT, RB == 2> ld;
+  // Eight-wave and two-block workgroups keep the loader's per-row angle constants in registers.
+  PLoader<D, KM, NT, RB == 2 || NW == 8> ld;
   ld.init(tid);
   TileIter<kSub> it;
   it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
