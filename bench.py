@@ -368,6 +368,14 @@ def main() -> int:
                                          dp.chunk_start, wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws),
                      args.steps, args.warmup)
 
+    # The same batch over a paged store (64-token blocks scattered over the pool, one record per block).
+    wpp = W.paginate(wp, 64, seed=7)
+    dpp = ops.upload(wpp, dev)
+    paged_ms = timed(lambda: ops.prefill(cfg, dpp.q, dpp.q_start, dpp.q_pos0, dpp.pool, dpp.pool, dpp.chunks,
+                                         dpp.chunk_start, wpp.max_q_len, wpp.max_kv_len, out=out, lse=lse,
+                                         workspace=ws), args.steps, args.warmup)
+    del dpp
+
     # Materialise-then-attend baseline: rotate-and-copy K, then plain attention over the copy.
     total_kv = int(wp.chunks["len"].astype(np.int64).sum())
     k_mat = torch.empty(cfg.num_kv_heads * total_kv * cfg.head_dim, dtype=torch.bfloat16, device=dev)
@@ -426,6 +434,7 @@ def main() -> int:
             "rotation_overhead": round(ms / norot_ms - 1.0, 4),
             "local_keys_ms": round(local_ms, 5),
             "local_keys_tflops": round(flops / (local_ms * 1e-3) / 1e12, 3),
+            "paged64_ms": round(paged_ms, 5),
             "materialize_ms": round(mat_ms, 5),
             "plain_attention_ms": round(plain_ms, 5),
             "materialize_then_attend_ms": round(mat_ms + plain_ms, 5),
@@ -469,6 +478,20 @@ def main() -> int:
                                                         out=outd, lse=lsed, workspace=wss), args.steps, args.warmup)
         item_keys = (plan.items["key_end"] - plan.items["key_begin"]).astype(np.int64)
         shared_read_mb = float(item_keys.sum()) * wd.num_kv_heads * wd.head_dim * 2 * 2 / 1e6
+        # The same batch over a paged store: 64-token blocks scattered over the pool, one record per block.
+        wpg = W.paginate(wd, 64, seed=7)
+        dpg = ops.upload(wpg, dev)
+        wspg = torch.empty(max(16, ops.decode_workspace_size(cfgd, wpg.batch, wpg.max_kv_len)), dtype=torch.uint8,
+                           device=dev)
+        dpaged = timed(lambda: ops.decode(cfgd, dpg.q, dpg.q_pos0, dpg.pool, dpg.pool, dpg.chunks, dpg.chunk_start,
+                                          wpg.max_kv_len, out=outd, lse=lsed, workspace=wspg), args.steps, args.warmup)
+        plan_pg = ops.upload_plan(ops.shared_decode_plan(cfgd, wpg.chunks, wpg.chunk_start), dev)
+        wss_pg = torch.empty(max(16, ops.decode_shared_workspace_size(cfgd, wpg.batch, plan_pg.max_slots)),
+                             dtype=torch.uint8, device=dev)
+        dpaged_shared = timed(lambda: ops.decode_shared(cfgd, dpg.q, dpg.q_pos0, dpg.pool, dpg.pool, plan_pg,
+                                                        out=outd, lse=lsed, workspace=wss_pg), args.steps,
+                              args.warmup)
+        del dpg, wspg, wss_pg
         tkv = int(wd.chunks["len"].astype(np.int64).sum())
         kmd = torch.empty(cfgd.num_kv_heads * tkv * cfgd.head_dim, dtype=torch.bfloat16, device=dev)
         chd = torch.empty_like(dd.chunks)
@@ -498,6 +521,8 @@ def main() -> int:
             "shared_items": int(plan.items.size),
             "shared_plan_host_ms": round(plan_ms, 3),
             "shared_speedup_vs_per_request": round(dms / dshared, 3),
+            "paged64_ms": round(dpaged, 5),
+            "paged64_shared_ms": round(dpaged_shared, 5),
             "materialize_ms": round(dmat, 5),
             "plain_decode_ms": round(dplain, 5),
             "materialize_then_attend_ms": round(dmat + dplain, 5),

@@ -376,6 +376,66 @@ def custom(seed: int, hq: int, hkv: int, d: int, base: float, requests, kind: st
                    [r["q_pos0"] for r in requests], rng, causal=causal, slack_fill=slack_fill)
 
 
+def paginate(w: Workload, block_tokens: int, seed: int = 0) -> Workload:
+    """Block-granular (paged) copy of a workload's store, as a paged KV allocator would hold it (Sec. 3.2 mentions
+    PagedAttention's block layout).  Every physical chunk is cut into blocks of ``block_tokens`` tokens; each block
+    stores ``K[Hkv][block_tokens][D]`` and ``V[Hkv][block_tokens][D]`` at its own place in a new pool, the blocks in
+    a random order.  Each record becomes one record per block it covers: len = the block's share of the record,
+    pos_offset = record offset + block start, strides = block_tokens.  Pure data movement: the attention inputs are
+    the same keys at the same positions (for a local-position store each block then holds keys at block-relative
+    local positions, which is a different but equally valid store)."""
+    rng = np.random.default_rng(seed)
+    hkv, d, bt = w.num_kv_heads, w.head_dim, int(block_tokens)
+    phys = {}
+    for rec in w.chunks:
+        key = (int(rec["k_offset"]), int(rec["v_offset"]))
+        phys[key] = max(phys.get(key, 0), int(rec["k_stride"]), int(rec["v_stride"]))
+    blocks = []  # (k_offset, v_offset, block index) of every block of every physical chunk
+    for (ko, vo), cap in phys.items():
+        for b in range(-(-cap // bt)):
+            blocks.append((ko, vo, b))
+    order = rng.permutation(len(blocks))
+    blk_elems = hkv * bt * d
+    pool = np.zeros(2 * blk_elems * len(blocks), dtype=np.float32)
+    where = {}
+    for slot, bi in enumerate(order):
+        ko, vo, b = blocks[bi]
+        where[(ko, vo, b)] = slot
+    new_recs = []
+    for rec in w.chunks:
+        ko, vo = int(rec["k_offset"]), int(rec["v_offset"])
+        n = int(rec["len"])
+        for b in range(-(-n // bt)):
+            slot = where[(ko, vo, b)]
+            nk = min(bt, n - b * bt)
+            new_recs.append((2 * slot * blk_elems, (2 * slot + 1) * blk_elems, nk, int(rec["pos_offset"]) + b * bt,
+                             bt, bt))
+    # copy the data block by block (whole capacity, so capacity slack travels with it)
+    recs_by_phys = {}
+    for rec in w.chunks:
+        recs_by_phys.setdefault((int(rec["k_offset"]), int(rec["v_offset"])), rec)
+    for (ko, vo, b), slot in where.items():
+        rec = recs_by_phys[(ko, vo)]
+        kst, vst = int(rec["k_stride"]), int(rec["v_stride"])
+        for base_old, st, base_new in ((ko, kst, 2 * slot * blk_elems), (vo, vst, (2 * slot + 1) * blk_elems)):
+            lo, hi = b * bt, min(st, (b + 1) * bt)
+            if hi <= lo:
+                continue
+            src = w.pool[base_old: base_old + hkv * st * d].reshape(hkv, st, d)[:, lo:hi, :]
+            dst = pool[base_new: base_new + blk_elems].reshape(hkv, bt, d)
+            dst[:, : hi - lo, :] = src
+    chunks = np.array(new_recs, dtype=CHUNK_DTYPE)
+    counts = []
+    for r in range(w.batch):
+        counts.append(sum(-(-int(rec["len"]) // bt) for rec in w.chunks[w.chunk_start[r]: w.chunk_start[r + 1]]))
+    chunk_start = np.zeros(w.batch + 1, dtype=np.int32)
+    chunk_start[1:] = np.cumsum(counts)
+    meta = dict(w.meta, block_tokens=bt, blocks=len(blocks))
+    return Workload(name=f"{w.name}_paged{bt}", kind=w.kind, num_q_heads=w.num_q_heads, num_kv_heads=hkv,
+                    head_dim=d, rope_base=w.rope_base, causal=w.causal, q=w.q, q_start=w.q_start, q_pos0=w.q_pos0,
+                    pool=pool, chunks=chunks, chunk_start=chunk_start, meta=meta)
+
+
 def by_name(name: str, **kw) -> Workload:
     table = {
         "tiny_rag_prefill": tiny_rag_prefill,

@@ -454,3 +454,25 @@ def test_shared_decode_full_size_sampled():
     ref_o, ref_l = oracle(w, requests=[0, 31, 63])
     rows = rows_of(w, [0, 31, 63])
     assert_close(out, None, ref_o, ref_l, rows, tag="shared full rag_decode")
+
+
+# --------------------------------------------------------------------------------------------------------------
+# Paged (block-granular) stores: each chunk's K/V in fixed-size blocks scattered over the pool, one record per
+# block.  The kernels see ordinary records (tiles never straddle a record); block sizes below a tile exercise the
+# partial-tile paths.
+@pytest.mark.parametrize("bt", [16, 64])
+@pytest.mark.parametrize("local", [False, True])
+def test_paged_prefill_matches_oracle(bt, local):
+    w = W.paginate(W.rag_prefill(seed=111, batch=3, hq=8, hkv=2, d=128, prefix_len=40, n_chunks=3, chunk_len=150,
+                                 pool_chunks=5, q_len=37), bt, seed=bt)
+    run_and_check(w, f"paged{bt} prefill {'local' if local else 'nope'}", LOCAL if local else {})
+
+
+@pytest.mark.parametrize("bt", [16, 32, 96])
+def test_paged_decode_matches_oracle_per_request_and_shared(bt):
+    w = W.paginate(W.rag_decode(seed=112, batch=6, hq=8, hkv=2, d=128, n_chunks=4, chunk_len=200, pool_chunks=5,
+                                tail_len=9, tail_cap=32), bt, seed=bt)
+    for local in (False, True):
+        ckw = LOCAL if local else {}
+        run_and_check(w, f"paged{bt} decode {'local' if local else 'nope'}", ckw)
+        run_shared_and_check(w, f"paged{bt} shared decode {'local' if local else 'nope'}", ckw)

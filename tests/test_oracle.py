@@ -465,3 +465,24 @@ def test_unknown_key_convention_is_rejected():
     w = W.tiny_rag_prefill(seed=0)
     with pytest.raises(ValueError):
         run(w, key_positions="absolute")
+
+
+def test_paged_store_is_the_same_attention():
+    """Paged (block-granular) copies of a store change only where keys live, not which keys sit at which positions:
+    the oracle's result is unchanged (prefill with a causal query chunk, decode with capacity slack)."""
+    w = W.rag_prefill(seed=31, batch=2, hq=4, hkv=2, d=16, prefix_len=7, n_chunks=3, chunk_len=50, pool_chunks=4,
+                      q_len=9)
+    for bt in (16, 64):
+        p = W.paginate(w, bt, seed=bt)
+        assert len(p.chunks) >= len(w.chunks) and p.meta["block_tokens"] == bt
+        assert bt > 50 or len(p.chunks) > len(w.chunks)
+        a, la = run(w)
+        b, lb = run(p)
+        np.testing.assert_array_equal(a, b)
+        np.testing.assert_array_equal(la, lb)
+    d = W.rag_decode(seed=32, batch=3, hq=4, hkv=2, d=16, n_chunks=2, chunk_len=70, pool_chunks=3, tail_len=5,
+                     tail_cap=40)
+    p = W.paginate(d, 32, seed=3)
+    a, _ = O.lazy_decode(d.q, d.q_pos0, d.pool, d.pool, d.chunks, d.chunk_start, 4, 2, 16, d.rope_base)
+    b, _ = O.lazy_decode(p.q, p.q_pos0, p.pool, p.pool, p.chunks, p.chunk_start, 4, 2, 16, p.rope_base)
+    np.testing.assert_array_equal(a, b)
