@@ -47,8 +47,10 @@ def rope_frequencies(head_dim: int, base: float, inv_freq=None) -> np.ndarray:
     return np.power(np.float64(base), -2.0 * t / head_dim)
 
 
-def rotate(x: np.ndarray, positions: np.ndarray, theta: np.ndarray) -> np.ndarray:
-    """Half-split rotary encoding R(p) of the last axis (Sec. 3.2 "Prefilling": one rotation of the two halves).
+def rotate(x: np.ndarray, positions: np.ndarray, theta: np.ndarray, pairing: str = "half") -> np.ndarray:
+    """Rotary encoding R(p) of the last axis.  Pair t is rotated by p * theta_t: (x_t, x_{t+D/2}) for the half-split
+    pairing of Sec. 3.2 "Prefilling" (the K1/K2 halves), (x_{2t}, x_{2t+1}) for the interleaved pairing used by
+    Llama (Sec. 3.5 "RoPE-family variants").
 
     x: [..., n, D] (any leading axes), positions: [n].  Returns fp64.
     """
@@ -56,8 +58,16 @@ def rotate(x: np.ndarray, positions: np.ndarray, theta: np.ndarray) -> np.ndarra
     half = x.shape[-1] // 2
     phi = np.asarray(positions, dtype=np.float64)[:, None] * theta[None, :]  # [n, D/2]
     c, s = np.cos(phi), np.sin(phi)
-    x1, x2 = x[..., :half], x[..., half:]
-    return np.concatenate([x1 * c - x2 * s, x1 * s + x2 * c], axis=-1)
+    if pairing == "half":
+        x1, x2 = x[..., :half], x[..., half:]
+        return np.concatenate([x1 * c - x2 * s, x1 * s + x2 * c], axis=-1)
+    if pairing == "interleaved":
+        x1, x2 = x[..., 0::2], x[..., 1::2]
+        y = np.empty_like(x)
+        y[..., 0::2] = x1 * c - x2 * s
+        y[..., 1::2] = x1 * s + x2 * c
+        return y
+    raise ValueError(f"unknown pairing {pairing!r}")
 
 
 def request_kv(pool_k, pool_v, chunks, lo: int, hi: int, num_kv_heads: int, head_dim: int,
@@ -139,11 +149,11 @@ def attend(q_rot, k_rot, v, q_pos, k_pos, causal: bool, scale: float):
 
 def lazy_attention(q, q_start, q_pos0, pool_k, pool_v, chunks, chunk_start, num_q_heads: int, num_kv_heads: int,
                    head_dim: int, rope_base: float, causal: bool = True, softmax_scale: float | None = None,
-                   inv_freq=None, requests=None, key_positions: str = "nope"):
+                   inv_freq=None, requests=None, key_positions: str = "nope", pairing: str = "half"):
     """Attention of every request's query tokens over its chunk table, keys re-encoded at their positions.
 
     q [total_q, Hq, D] (NoPE queries), q_start [B+1], q_pos0 [B]: token i of request r is at q_pos0[r] + i.
-    key_positions: "nope" or "local" store convention (module docstring).
+    key_positions: "nope" or "local" store convention (module docstring); pairing: "half" or "interleaved".
     Returns out [total_q, Hq, D] and lse [total_q, Hq] in fp64.  ``requests`` restricts the work to a subset of
     request indices (other rows stay 0 / -inf).
     """
@@ -161,8 +171,8 @@ def lazy_attention(q, q_start, q_pos0, pool_k, pool_v, chunks, chunk_start, num_
         k, v, kpos, offs = request_kv(pool_k, pool_v, chunks, int(chunk_start[r]), int(chunk_start[r + 1]),
                                       num_kv_heads, head_dim, with_offsets=True)
         qpos = int(q_pos0[r]) + np.arange(b - a, dtype=np.int64)
-        k_rot = rotate(k, key_rotation_positions(kpos, offs, key_positions), theta)  # explicit re-encoded copy
-        q_rot = rotate(np.swapaxes(np.asarray(q[a:b], dtype=np.float64), 0, 1), qpos, theta)  # [Hq, Lq, D]
+        k_rot = rotate(k, key_rotation_positions(kpos, offs, key_positions), theta, pairing)  # re-encoded copy
+        q_rot = rotate(np.swapaxes(np.asarray(q[a:b], dtype=np.float64), 0, 1), qpos, theta, pairing)  # [Hq, Lq, D]
         o, l = attend(np.swapaxes(q_rot, 0, 1), k_rot, v, qpos, kpos, causal, scale)
         out[a:b] = o
         lse[a:b] = l
@@ -170,16 +180,17 @@ def lazy_attention(q, q_start, q_pos0, pool_k, pool_v, chunks, chunk_start, num_
 
 
 def lazy_decode(q, q_pos, pool_k, pool_v, chunks, chunk_start, num_q_heads, num_kv_heads, head_dim, rope_base,
-                causal=True, softmax_scale=None, inv_freq=None, requests=None, key_positions: str = "nope"):
+                causal=True, softmax_scale=None, inv_freq=None, requests=None, key_positions: str = "nope",
+                pairing: str = "half"):
     """One query token per request at q_pos[r] (decode, Sec. 3.2 "Decoding"): q [B, Hq, D]."""
     batch = len(q_pos)
     q_start = np.arange(batch + 1)
     return lazy_attention(q, q_start, q_pos, pool_k, pool_v, chunks, chunk_start, num_q_heads, num_kv_heads,
-                          head_dim, rope_base, causal, softmax_scale, inv_freq, requests, key_positions)
+                          head_dim, rope_base, causal, softmax_scale, inv_freq, requests, key_positions, pairing)
 
 
 def materialize_k(pool_k, chunks, chunk_start, num_kv_heads: int, head_dim: int, rope_base: float, inv_freq=None,
-                  key_positions: str = "nope"):
+                  key_positions: str = "nope", pairing: str = "half"):
     """Re-encoded key copy of every request (the materialise-then-attend baseline's first step): a list over
     requests of K' [Hkv, L_r, D], keys in chunk-table order, each encoded at pos_offset + j."""
     theta = rope_frequencies(head_dim, rope_base, inv_freq)
@@ -187,7 +198,7 @@ def materialize_k(pool_k, chunks, chunk_start, num_kv_heads: int, head_dim: int,
     for r in range(len(chunk_start) - 1):
         k, _, kpos, offs = request_kv(pool_k, pool_k, chunks, int(chunk_start[r]), int(chunk_start[r + 1]),
                                       num_kv_heads, head_dim, with_offsets=True)
-        res.append(rotate(k, key_rotation_positions(kpos, offs, key_positions), theta))
+        res.append(rotate(k, key_rotation_positions(kpos, offs, key_positions), theta, pairing))
     return res
 
 

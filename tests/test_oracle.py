@@ -486,3 +486,61 @@ def test_paged_store_is_the_same_attention():
     a, _ = O.lazy_decode(d.q, d.q_pos0, d.pool, d.pool, d.chunks, d.chunk_start, 4, 2, 16, d.rope_base)
     b, _ = O.lazy_decode(p.q, p.q_pos0, p.pool, p.pool, p.chunks, p.chunk_start, 4, 2, 16, p.rope_base)
     np.testing.assert_array_equal(a, b)
+
+
+# ---------------------------------------------------------------------------------------------------------------
+# Interleaved RoPE pairing (Sec. 3.5 "RoPE-family variants": pairs (2t, 2t+1), as used by Llama).
+# ---------------------------------------------------------------------------------------------------------------
+def test_interleaved_pairing_brute_force():
+    """Pure-Python complex arithmetic, z_t = x_{2t} + i x_{2t+1} rotated by exp(i p theta_t), on decode lse."""
+    d, base = 8, 1.0e4
+    reqs = [dict(chunks=[(6, 3), (4, 20)], q_len=1, q_pos0=31)]
+    w = W.custom(41, 1, 1, d, base, reqs, kind="decode")
+    _, lse = O.lazy_decode(w.q, w.q_pos0, w.pool, w.pool, w.chunks, w.chunk_start, 1, 1, d, base,
+                           pairing="interleaved")
+    th = [base ** (-2.0 * t / d) for t in range(d // 2)]
+    m = int(w.q_pos0[0])
+    q = [complex(float(w.q[0, 0, 2 * t]), float(w.q[0, 0, 2 * t + 1])) * cmath.exp(1j * m * th[t])
+         for t in range(d // 2)]
+    scores = []
+    for rec in w.chunks:
+        for j in range(int(rec["len"])):
+            a = int(rec["k_offset"]) + j * d
+            p = int(rec["pos_offset"]) + j
+            k = [complex(float(w.pool[a + 2 * t]), float(w.pool[a + 2 * t + 1])) * cmath.exp(1j * p * th[t])
+                 for t in range(d // 2)]
+            scores.append(sum((q[t].conjugate() * k[t]).real for t in range(d // 2)) / math.sqrt(d))
+    mx = max(scores)
+    ref = mx + math.log(sum(math.exp(s - mx) for s in scores))
+    assert abs(lse[0, 0] - ref) < 1e-12
+
+
+def test_interleaved_equals_half_split_on_permuted_queries_and_keys():
+    """Interleaved RoPE on (q, k) is half-split RoPE on (P q, P k) with P: 2t -> t, 2t+1 -> t + D/2 (values are not
+    permuted).  Both key conventions."""
+    w = W.rag_prefill(seed=42, batch=2, hq=4, hkv=2, d=16, prefix_len=5, n_chunks=3, chunk_len=11, pool_chunks=4,
+                      q_len=6)
+    d = w.head_dim
+    perm = np.concatenate([np.arange(0, d, 2), np.arange(1, d, 2)])  # new index t holds old index perm[t]
+    pool = w.pool.copy()
+    done = set()
+    for rec in w.chunks:
+        ko, cap = int(rec["k_offset"]), int(rec["k_stride"])
+        if ko in done:
+            continue
+        done.add(ko)
+        blk = pool[ko: ko + w.num_kv_heads * cap * d].reshape(-1, d)
+        blk[:] = blk[:, perm]
+    q = w.q[..., perm]
+    for kp in ("nope", "local"):
+        a, la = O.lazy_attention(w.q, w.q_start, w.q_pos0, w.pool, w.pool, w.chunks, w.chunk_start, 4, 2, d,
+                                 w.rope_base, key_positions=kp, pairing="interleaved")
+        b, lb = O.lazy_attention(q, w.q_start, w.q_pos0, pool, pool, w.chunks, w.chunk_start, 4, 2, d, w.rope_base,
+                                 key_positions=kp, pairing="half")
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(la, lb, rtol=0, atol=1e-11)
+
+
+def test_unknown_pairing_is_rejected():
+    with pytest.raises(ValueError):
+        O.rotate(np.zeros((1, 4)), np.zeros(1), np.ones(2), pairing="swapped")
