@@ -13,8 +13,9 @@
  *    null stream).  Inputs are read-only; in particular the chunk store is never written, so concurrent requests
  *    that share a chunk cannot race (Sec. 1: in-place re-encoding races when two prompts share data).
  *  - Element type of q, k, v and out is bfloat16 (raw 16-bit storage, passed as void*); accumulation is fp32.
- *  - head_dim D is 64 or 128.  RoPE pairs dimension t with t + D/2 (half-split, the K1/K2 halves of Sec. 3.2
- *    "Prefilling"): x1' = x1 cos(p theta_t) - x2 sin(p theta_t), x2' = x1 sin(p theta_t) + x2 cos(p theta_t),
+ *  - head_dim D is 64 or 128.  RoPE pairs dimension t with t + D/2 by default (half-split, the K1/K2 halves of
+ *    Sec. 3.2 "Prefilling"; params->rope_style selects the interleaved pairs (2t, 2t+1) instead):
+ *    x1' = x1 cos(p theta_t) - x2 sin(p theta_t), x2' = x1 sin(p theta_t) + x2 cos(p theta_t),
  *    theta_t = rope_base^(-2t/D) unless params->inv_freq supplies the D/2 frequencies (RoPE variants, Sec. 3.5).
  *  - GQA: query head h reads KV head h / (num_q_heads / num_kv_heads) (Sec. 3.5).
  *  - Causal rule: a key at position pk is visible to a query at position pq iff pk <= pq (positions, not table
@@ -79,7 +80,19 @@ typedef struct lazy_attn_params {
   const float* inv_freq; /* optional device array of D/2 fp32 frequencies theta_t (scaled / NTK tables) */
   int32_t num_splits;    /* 0 => chosen by the library; otherwise the number of KV splits per request */
   int32_t key_positions; /* LAZY_KEYS_NOPE or LAZY_KEYS_LOCAL: how the chunk store holds its keys (below) */
+  int32_t rope_style;    /* LAZY_ROPE_HALF or LAZY_ROPE_INTERLEAVED: which dimensions form a rotation pair */
+  int32_t reserved;      /* must be 0 */
 } lazy_attn_params_t;
+
+/*
+ * Rotation pairs (params->rope_style; Sec. 3.5 "RoPE-family variants").  Pair t (0 <= t < D/2) is rotated by
+ * p * theta_t in both styles:
+ *  LAZY_ROPE_HALF        (0): pair t = dimensions (t, t + D/2), the K1/K2 halves of Sec. 3.2 "Prefilling".
+ *  LAZY_ROPE_INTERLEAVED (1): pair t = dimensions (2t, 2t + 1), as in Llama's reference implementation.
+ * Q, K and the materialised copy follow the style; V and the output are not affected.
+ */
+#define LAZY_ROPE_HALF 0
+#define LAZY_ROPE_INTERLEAVED 1
 
 /*
  * Key-store conventions (params->key_positions).  Values and the causal rule are the same in both; only the

@@ -21,6 +21,8 @@ int check_params(const lazy_attn_params_t* p) {
   if (!p->inv_freq && !(isfinite(p->rope_base) && p->rope_base > 0.f)) return LAZY_EINVAL;
   if (p->num_splits < 0) return LAZY_EINVAL;
   if (p->key_positions != LAZY_KEYS_NOPE && p->key_positions != LAZY_KEYS_LOCAL) return LAZY_EINVAL;
+  if (p->rope_style != LAZY_ROPE_HALF && p->rope_style != LAZY_ROPE_INTERLEAVED) return LAZY_EINVAL;
+  if (p->reserved != 0) return LAZY_EINVAL;
   if (p->head_dim != 64 && p->head_dim != 128) return LAZY_EUNSUPPORTED;
   return LAZY_OK;
 }
@@ -135,6 +137,7 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
   a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
+  a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
   return status(lazy::launch_prefill(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
 
@@ -180,6 +183,7 @@ int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const 
   a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
+  a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
   return status(lazy::launch_decode(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
 
@@ -257,6 +261,7 @@ int lazy_materialize_k(const lazy_attn_params_t* params, const void* k_pool, con
                                          params->num_kv_heads, params->head_dim,
                                          params->inv_freq ? 0.0 : log2((double)params->rope_base),
                                          params->inv_freq, params->key_positions == LAZY_KEYS_LOCAL,
+                                         params->rope_style == LAZY_ROPE_INTERLEAVED,
                                          static_cast<uint16_t*>(k_out), chunks_out,
                                          static_cast<hipStream_t>(stream)));
 }
@@ -300,6 +305,7 @@ int lazy_attn_decode_shared(const lazy_attn_params_t* p, const void* q, const in
   a.group = p->num_q_heads / p->num_kv_heads;
   a.causal = p->causal;
   a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
+  a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
   a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   return status(lazy::launch_decode_shared(a, num_items, max_slots, slot_start, p->head_dim,

@@ -33,6 +33,7 @@ struct AttnArgs {
   int32_t row_blocks;         // prefill: a workgroup covers 128 * row_blocks packed rows (2 = eight-wave kernel)
   int32_t head_groups;        // decode: ceil(group / 16)
   int32_t local_keys;         // 1: the store holds keys encoded at local positions (LAZY_KEYS_LOCAL)
+  int32_t interleaved;        // 1: RoPE pairs (2t, 2t+1) (LAZY_ROPE_INTERLEAVED)
   double rope_log2_base;      // log2(rope_base), computed on the host (unused with inv_freq)
   float scale_log2;           // softmax scale * log2(e)
 };
@@ -54,6 +55,7 @@ struct SharedArgs {
   int32_t group;
   int32_t causal;
   int32_t local_keys;
+  int32_t interleaved;
   double rope_log2_base;
   float scale_log2;
 };
@@ -72,7 +74,7 @@ hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int spl
                           uint16_t* out, float* lse, hipStream_t stream);
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
                               int max_chunk_len, int hkv, int head_dim, double rope_log2_base, const float* inv_freq,
-                              bool local_keys,
+                              bool local_keys, bool interleaved,
                               uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t stream);
 
 }  // namespace lazy

@@ -136,6 +136,27 @@ __device__ __forceinline__ void rotate_by(float x1, float x2, float2 cs, float& 
 // materialise-then-attend baseline), NoPE keys rotated at pos_offset + j, or local-position keys (stored encoded at
 // j) rotated by the record's pos_offset.
 constexpr int kKeysPlain = 0, kKeysNope = 1, kKeysLocal = 2;
+// Bit 2 of a kernel's key-mode argument selects the interleaved pairing (pairs (2t, 2t+1)).  Interleaved RoPE on
+// (q, k) is the half-split rotation of (P q, P k) for the permutation P: 2t -> t, 2t+1 -> t + D/2 (V unchanged), so
+// the kernels only change their Q and K loads: 16 consecutive elements are split into the pairs' first and second
+// halves, the layout a half-split load produces, and everything after the load is shared.
+constexpr int kInterleaved = 4;
+constexpr int keys_of(int km) { return km & 3; }
+constexpr bool interleaved_of(int km) { return (km & kInterleaved) != 0; }
+
+// 16 bf16 = pairs t0..t0+7 of an interleaved vector (w0: pairs t0..t0+3, one pair per 32-bit word, first element
+// in the low half; w1: pairs t0+4..t0+7) -> the first elements (lo) and second elements (hi) in pair order.
+__device__ __forceinline__ void deinterleave8(u32x4 w0, u32x4 w1, u32x4& lo, u32x4& hi) {
+  lo = u32x4{(w0[0] & 0xffffu) | (w0[1] << 16), (w0[2] & 0xffffu) | (w0[3] << 16), (w1[0] & 0xffffu) | (w1[1] << 16),
+             (w1[2] & 0xffffu) | (w1[3] << 16)};
+  hi = u32x4{(w0[0] >> 16) | (w0[1] & 0xffff0000u), (w0[2] >> 16) | (w0[3] & 0xffff0000u),
+             (w1[0] >> 16) | (w1[1] & 0xffff0000u), (w1[2] >> 16) | (w1[3] & 0xffff0000u)};
+}
+// Four pairs: 8 bf16 of an interleaved vector -> first and second elements.
+__device__ __forceinline__ void deinterleave4(u32x4 w, u32x2& lo, u32x2& hi) {
+  lo = u32x2{(w[0] & 0xffffu) | (w[1] << 16), (w[2] & 0xffffu) | (w[3] << 16)};
+  hi = u32x2{(w[0] >> 16) | (w[1] & 0xffff0000u), (w[2] >> 16) | (w[3] & 0xffff0000u)};
+}
 
 // Rotate a query pair at position p (accurate angle per pair).
 __device__ __forceinline__ void rotate_q_pair(float x1, float x2, int p, double rev, float& y1, float& y2) {
@@ -356,10 +377,11 @@ __device__ __forceinline__ int kblk_t(int b) {
 // each rotating PP = D / (2 TPR) pairs of its row; V copied row-major in 16-byte chunks (VC per thread, of the same
 // row, so that a thread's share of K and V is one key row: threads 0..NT/2-1 hold rows 0..31).
 // The per-row cos/sin constants are written to a private LDS slice once per workgroup and read per tile.
-template <int D, int KM, int NT, bool CSD_REGS = false>
+template <int D, int KMI, int NT, bool CSD_REGS = false>
 struct PLoader {
   using S = TileLayout<D>;
-  static constexpr bool ROT = KM != kKeysPlain, LOCAL = KM == kKeysLocal;
+  static constexpr int KM = keys_of(KMI);
+  static constexpr bool ROT = KM != kKeysPlain, LOCAL = KM == kKeysLocal, IL = interleaved_of(KMI);
   static constexpr int TPR = NT / kSub;
   static constexpr int PP = D / (2 * TPR);
   static constexpr int NV = PP / 8;
@@ -389,11 +411,17 @@ struct PLoader {
   __device__ void fetch(const uint16_t* kbase, const uint16_t* vbase, int nvalid) {
     const u32x4 zero = {0, 0, 0, 0};
     if (nvalid >= kSub) {
-      const uint16_t* src = kbase + (size_t)row * D + part * PP;
+      if (IL) {
+        const u32x4* src = reinterpret_cast<const u32x4*>(kbase + (size_t)row * D + 2 * part * PP);
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        klo[v] = reinterpret_cast<const u32x4*>(src)[v];
-        khi[v] = reinterpret_cast<const u32x4*>(src + D / 2)[v];
+        for (int v = 0; v < NV; ++v) deinterleave8(src[2 * v], src[2 * v + 1], klo[v], khi[v]);
+      } else {
+        const uint16_t* src = kbase + (size_t)row * D + part * PP;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          klo[v] = reinterpret_cast<const u32x4*>(src)[v];
+          khi[v] = reinterpret_cast<const u32x4*>(src + D / 2)[v];
+        }
       }
 #pragma unroll
       for (int i = 0; i < VC; ++i)
@@ -401,11 +429,17 @@ struct PLoader {
       return;
     }
     const bool ok = row < nvalid;
-    const uint16_t* src = kbase + (size_t)(ok ? row : 0) * D + part * PP;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
-      const u32x4 lo = reinterpret_cast<const u32x4*>(src)[v];
-      const u32x4 hi = reinterpret_cast<const u32x4*>(src + D / 2)[v];
+      u32x4 lo, hi;
+      if (IL) {
+        const u32x4* src = reinterpret_cast<const u32x4*>(kbase + (size_t)(ok ? row : 0) * D + 2 * part * PP);
+        deinterleave8(src[2 * v], src[2 * v + 1], lo, hi);
+      } else {
+        const uint16_t* src = kbase + (size_t)(ok ? row : 0) * D + part * PP;
+        lo = reinterpret_cast<const u32x4*>(src)[v];
+        hi = reinterpret_cast<const u32x4*>(src + D / 2)[v];
+      }
       klo[v] = ok ? lo : zero;
       khi[v] = ok ? hi : zero;
     }
@@ -596,11 +630,12 @@ __device__ __forceinline__ void attend_tile(const uint16_t* kb, const uint16_t* 
   __builtin_amdgcn_s_setprio(0);
 }
 
-template <int D, int KM, int NW, int NBUF, int RB>
+template <int D, int KMI, int NW, int NBUF, int RB>
 __global__ __launch_bounds__(NW * 64)
 __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void prefill_kernel(AttnArgs a) {
   __shared__ PrefillSmem<D, NBUF> sm;
-  constexpr bool ROT = KM != kKeysPlain, LOCAL = KM == kKeysLocal;
+  constexpr int KM = keys_of(KMI);
+  constexpr bool ROT = KM != kKeysPlain, LOCAL = KM == kKeysLocal, IL = interleaved_of(KMI);
   using S = TileLayout<D>;
   constexpr int NT = NW * 64;
   constexpr int BM = 32 * NW * RB;
@@ -643,13 +678,17 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
       const int t0 = 8 * s + 4 * h2;
       qraw[rb][s][0] = qraw[rb][s][1] = u32x2{0, 0};
       if (rvalid[rb]) {
-        qraw[rb][s][0] = *reinterpret_cast<const u32x2*>(qrow + t0);
-        qraw[rb][s][1] = *reinterpret_cast<const u32x2*>(qrow + D / 2 + t0);
+        if (IL) {
+          deinterleave4(*reinterpret_cast<const u32x4*>(qrow + 2 * t0), qraw[rb][s][0], qraw[rb][s][1]);
+        } else {
+          qraw[rb][s][0] = *reinterpret_cast<const u32x2*>(qrow + t0);
+          qraw[rb][s][1] = *reinterpret_cast<const u32x2*>(qrow + D / 2 + t0);
+        }
       }
     }
   }
   // Eight-wave and two-block workgroups keep the loader's per-row angle constants in registers.
-  PLoader<D, KM, NT, RB == 2 || NW == 8> ld;
+  PLoader<D, KMI, NT, RB == 2 || NW == 8> ld;
   ld.init(tid);
   TileIter<kSub> it;
   it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
@@ -810,7 +849,32 @@ struct DecTile {
   u32x4 v[VC];
 };
 
-template <int D>
+// One key row's k-step pair s for this lane (pairs 32 s + 8 kq .. +7): first elements in lo, second in hi for
+// the half-split pairing; for the interleaved pairing the raw 16 elements (pairs_of splits them where they are
+// used, so that tiles in flight hold no extra registers).
+template <int D, bool IL>
+__device__ __forceinline__ void dec_k_pairs(const uint16_t* krow, int s, int kq, u32x4& lo, u32x4& hi) {
+  if (IL) {
+    const u32x4* src = reinterpret_cast<const u32x4*>(krow + 2 * (32 * s + 8 * kq));
+    lo = src[0];
+    hi = src[1];
+  } else {
+    lo = *reinterpret_cast<const u32x4*>(krow + 32 * s + 8 * kq);
+    hi = *reinterpret_cast<const u32x4*>(krow + D / 2 + 32 * s + 8 * kq);
+  }
+}
+
+template <bool IL>
+__device__ __forceinline__ void pairs_of(u32x4 a, u32x4 b, u32x4& lo, u32x4& hi) {
+  if (IL) {
+    deinterleave8(a, b, lo, hi);
+  } else {
+    lo = a;
+    hi = b;
+  }
+}
+
+template <int D, bool IL>
 __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, const uint16_t* vbase, int nvalid,
                                           int lane) {
   const int r = lane & 15, kq = lane >> 4;
@@ -818,12 +882,9 @@ __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, 
   if (nvalid >= kDecWaveKeys) {
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-      const uint16_t* row = kbase + (size_t)kappa(b, r) * D + 8 * kq;
+      const uint16_t* row = kbase + (size_t)kappa(b, r) * D;
 #pragma unroll
-      for (int s = 0; s < DecTile<D>::SP; ++s) {
-        t.k[b][s][0] = *reinterpret_cast<const u32x4*>(row + 32 * s);
-        t.k[b][s][1] = *reinterpret_cast<const u32x4*>(row + D / 2 + 32 * s);
-      }
+      for (int s = 0; s < DecTile<D>::SP; ++s) dec_k_pairs<D, IL>(row, s, kq, t.k[b][s][0], t.k[b][s][1]);
     }
 #pragma unroll
     for (int i = 0; i < DecTile<D>::VC; ++i) {
@@ -836,11 +897,11 @@ __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, 
   for (int b = 0; b < 2; ++b) {
     const int key = kappa(b, r);
     const bool ok = key < nvalid;
-    const uint16_t* row = kbase + (size_t)(ok ? key : 0) * D + 8 * kq;
+    const uint16_t* row = kbase + (size_t)(ok ? key : 0) * D;
 #pragma unroll
     for (int s = 0; s < DecTile<D>::SP; ++s) {
-      const u32x4 lo = *reinterpret_cast<const u32x4*>(row + 32 * s);
-      const u32x4 hi = *reinterpret_cast<const u32x4*>(row + D / 2 + 32 * s);
+      u32x4 lo, hi;
+      dec_k_pairs<D, IL>(row, s, kq, lo, hi);
       t.k[b][s][0] = ok ? lo : zero;
       t.k[b][s][1] = ok ? hi : zero;
     }
@@ -859,7 +920,7 @@ __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, 
 // of the tile, per-row rows cd0 / cd1 of blocks 0 / 1) and S^T = K Q^T, the key mask, the online-softmax update
 // and O^T += V^T P^T.  lim: this lane's visible keys are the tile keys kk < lim (tile tail and causal rule; it may
 // differ between the lanes' columns).
-template <int D, bool ROT>
+template <int D, bool ROT, bool IL>
 __device__ __forceinline__ void dec_tile(const DecTile<D>& cur, uint16_t* vw, const uint16_t* vlane, const float* cb,
                                          const float* cd0, const float* cd1, const bf16x8 (&qf)[D / 32],
                                          f32x4 (&o)[D / 16], float& m2, float& lsum, int lim, float c, int lane) {
@@ -879,7 +940,8 @@ __device__ __forceinline__ void dec_tile(const DecTile<D>& cur, uint16_t* vw, co
   for (int s = 0; s < SP; ++s) {
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-      const u32x4 wl = cur.k[b][s][0], wh = cur.k[b][s][1];
+      u32x4 wl, wh;
+      pairs_of<IL>(cur.k[b][s][0], cur.k[b][s][1], wl, wh);
       u32x4 klo, khi;
       if (ROT) {
         const float* cdb = b ? cd1 : cd0;
@@ -948,9 +1010,11 @@ __device__ __forceinline__ void dec_tile(const DecTile<D>& cur, uint16_t* vw, co
   }
 }
 
-template <int D, int KM>
+template <int D, int KMI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_kernel(AttnArgs a) {
   __shared__ DecodeSmem<D> sm;
+  constexpr int KM = keys_of(KMI);
+  constexpr bool IL = interleaved_of(KMI);
   // Keys are rotated in registers only for a NoPE store; with local-position keys the query is rotated by the
   // relative offset q_pos - pos_offset whenever the record changes (Sec. 3.2 "Decoding") and the keys are used as
   // stored.
@@ -975,12 +1039,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const uint16_t* qrow = a.q + ((int64_t)r * a.hq + head) * D;
 #pragma unroll
     for (int s = 0; s < SP; ++s) {
-      const int t0 = 32 * s + 8 * kq;
       qraw[s][0] = qraw[s][1] = u32x4{0, 0, 0, 0};
-      if (hvalid) {
-        qraw[s][0] = *reinterpret_cast<const u32x4*>(qrow + t0);
-        qraw[s][1] = *reinterpret_cast<const u32x4*>(qrow + D / 2 + t0);
-      }
+      if (hvalid) dec_k_pairs<D, IL>(qrow, s, kq, qraw[s][0], qraw[s][1]);
     }
   }
   // This wave's tiles: every fourth tile of the split, starting at tile `wave`.
@@ -990,7 +1050,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   bool have = it.seek(a.causal, qpos);
   DecTile<D> cur, nxt;
   if (have)
-    dec_fetch<D>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+    dec_fetch<D, IL>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
                  min(kDecWaveKeys, it.cur.len - it.j0), lane);
 
   if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
@@ -1012,10 +1072,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int s = 0; s < SP; ++s) {
       float y1[8], y2[8];
       const int t0 = 32 * s + 8 * kq;
+      u32x4 ql, qh;
+      pairs_of<IL>(qraw[s][0], qraw[s][1], ql, qh);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float x1 = (e & 1) ? bf_hi(qraw[s][0][e >> 1]) : bf_lo(qraw[s][0][e >> 1]);
-        const float x2 = (e & 1) ? bf_hi(qraw[s][1][e >> 1]) : bf_lo(qraw[s][1][e >> 1]);
+        const float x1 = (e & 1) ? bf_hi(ql[e >> 1]) : bf_lo(ql[e >> 1]);
+        const float x2 = (e & 1) ? bf_hi(qh[e >> 1]) : bf_lo(qh[e >> 1]);
         rotate_q_pair(x1, x2, qpos, sm.freq[t0 + e], y1[e], y2[e]);
       }
       qf[2 * s] =
@@ -1059,7 +1121,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
       for (int s = 0; s < SP; ++s) {
         float y1[8], y2[8];
-        const u32x4 ql = sm.qsave[s][0][lane], qh = sm.qsave[s][1][lane];
+        u32x4 ql, qh;
+        pairs_of<IL>(sm.qsave[s][0][lane], sm.qsave[s][1][lane], ql, qh);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float x1 = (e & 1) ? bf_hi(ql[e >> 1]) : bf_lo(ql[e >> 1]);
@@ -1076,7 +1139,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int k = 0; k < 4 && it.left > 0; ++k) it.step();
     const bool have_next = it.seek(a.causal, qpos);
     if (have_next) {
-      dec_fetch<D>(nxt, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+      dec_fetch<D, IL>(nxt, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
                    min(kDecWaveKeys, it.cur.len - it.j0), lane);
       if (ROT && lane < D / 2)
         *reinterpret_cast<float2*>(sm.csb[wave][buf ^ 1] + csb_idx<D>(lane)) =
@@ -1084,7 +1147,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
 
     const int lim = min(nvalid, a.causal ? qpos - b0 + 1 : kDecWaveKeys);
-    dec_tile<D, ROT>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane);
+    dec_tile<D, ROT, IL>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane);
     cur = nxt;
     buf ^= 1;
     have = have_next;
@@ -1147,9 +1210,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 // j <= rel under the causal rule.  Waves take the range's 32-key tiles w, w + 4, ... with the next tile in flight,
 // as in decode_kernel, and every (user, item) writes one partial result into its request's slot.
 // ---------------------------------------------------------------------------------------------------------------
-template <int D, int KM>
+template <int D, int KMI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_shared_kernel(
     SharedArgs a) {
+  constexpr int KM = keys_of(KMI);
+  constexpr bool IL = interleaved_of(KMI);
   __shared__ DecodeSmem<D> sm;
   __shared__ float ucs[16][DecodeSmem<D>::CSB];  // per user: cos/sin(rel theta_t) at csb_idx(t)
   using S = DecodeSmem<D>;
@@ -1175,12 +1240,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const uint16_t* qrow = a.q + ((int64_t)usr.request * a.hq + g * G + col % G) * D;
 #pragma unroll
     for (int s = 0; s < SP; ++s) {
-      const int t0 = 32 * s + 8 * kq;
       qraw[s][0] = qraw[s][1] = u32x4{0, 0, 0, 0};
-      if (cvalid) {
-        qraw[s][0] = *reinterpret_cast<const u32x4*>(qrow + t0);
-        qraw[s][1] = *reinterpret_cast<const u32x4*>(qrow + D / 2 + t0);
-      }
+      if (cvalid) dec_k_pairs<D, IL>(qrow, s, kq, qraw[s][0], qraw[s][1]);
     }
   }
   const uint16_t* kbase = a.k_pool + koff + (int64_t)g * kst * D;
@@ -1190,7 +1251,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   DecTile<D> cur, nxt;
   if (tile < ntiles) {
     const int j0 = kb + kDecWaveKeys * tile;
-    dec_fetch<D>(cur, kbase + (int64_t)j0 * D, vbase + (int64_t)j0 * D, min(kDecWaveKeys, ke - j0), lane);
+    dec_fetch<D, IL>(cur, kbase + (int64_t)j0 * D, vbase + (int64_t)j0 * D, min(kDecWaveKeys, ke - j0), lane);
   }
 
   if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
@@ -1216,10 +1277,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
   for (int s = 0; s < SP; ++s) {
     float y1[8], y2[8];
+    u32x4 ql, qh;
+    pairs_of<IL>(qraw[s][0], qraw[s][1], ql, qh);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float x1 = (e & 1) ? bf_hi(qraw[s][0][e >> 1]) : bf_lo(qraw[s][0][e >> 1]);
-      const float x2 = (e & 1) ? bf_hi(qraw[s][1][e >> 1]) : bf_lo(qraw[s][1][e >> 1]);
+      const float x1 = (e & 1) ? bf_hi(ql[e >> 1]) : bf_lo(ql[e >> 1]);
+      const float x2 = (e & 1) ? bf_hi(qh[e >> 1]) : bf_lo(qh[e >> 1]);
       rotate_by(x1, x2, *reinterpret_cast<const float2*>(&ucs[cuser][csb_idx<D>(32 * s + 8 * kq + e)]), y1[e],
                 y2[e]);
     }
@@ -1244,12 +1307,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int next = tile + 4;
     if (next < ntiles) {
       const int j1 = kb + kDecWaveKeys * next;
-      dec_fetch<D>(nxt, kbase + (int64_t)j1 * D, vbase + (int64_t)j1 * D, min(kDecWaveKeys, ke - j1), lane);
+      dec_fetch<D, IL>(nxt, kbase + (int64_t)j1 * D, vbase + (int64_t)j1 * D, min(kDecWaveKeys, ke - j1), lane);
       if (ROT && lane < D / 2)
         *reinterpret_cast<float2*>(sm.csb[wave][buf ^ 1] + csb_idx<D>(lane)) = rope_cs(j1, sm.freq[lane]);
     }
     const int lim = min(nvalid, a.causal ? rel - j0 + 1 : kDecWaveKeys);
-    dec_tile<D, ROT>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane);
+    dec_tile<D, ROT, IL>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane);
     cur = nxt;
     buf ^= 1;
     tile = next;
@@ -1404,7 +1467,7 @@ __global__ __launch_bounds__(kThreads) void materialize_plan_kernel(const lazy_c
 
 // Rotate-and-copy: workgroup = (64-key sub-tile, KV head, record).  Same angle decomposition and rounding as the
 // lazy loader, written back in the natural head-dimension order.
-template <int D, bool LOCAL>
+template <int D, bool LOCAL, bool IL>
 __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint16_t* __restrict__ k_pool,
                                                                       const lazy_chunk_t* __restrict__ in,
                                                                       const lazy_chunk_t* __restrict__ plan,
@@ -1431,8 +1494,14 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
     const int t0 = quarter * PP + 8 * v;
-    const u32x4 wl = *reinterpret_cast<const u32x4*>(src + t0);
-    const u32x4 wh = *reinterpret_cast<const u32x4*>(src + D / 2 + t0);
+    u32x4 wl, wh;
+    if (IL) {
+      deinterleave8(reinterpret_cast<const u32x4*>(src + 2 * t0)[0], reinterpret_cast<const u32x4*>(src + 2 * t0)[1],
+                    wl, wh);
+    } else {
+      wl = *reinterpret_cast<const u32x4*>(src + t0);
+      wh = *reinterpret_cast<const u32x4*>(src + D / 2 + t0);
+    }
     float yl[8], yh[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -1443,10 +1512,17 @@ __global__ __launch_bounds__(kThreads) void materialize_rotate_kernel(const uint
       else
         rotate_pair(x1, x2, cs[row / kAngleRows][t0 + e], rope_cs(row % kAngleRows, freq[t0 + e]), yl[e], yh[e]);
     }
-    *reinterpret_cast<u32x4*>(dst + t0) =
-        u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yl[4], yl[5]), pack2(yl[6], yl[7])};
-    *reinterpret_cast<u32x4*>(dst + D / 2 + t0) =
-        u32x4{pack2(yh[0], yh[1]), pack2(yh[2], yh[3]), pack2(yh[4], yh[5]), pack2(yh[6], yh[7])};
+    if (IL) {  // written back interleaved: pair t0 + e at elements 2 (t0 + e), 2 (t0 + e) + 1
+      *reinterpret_cast<u32x4*>(dst + 2 * t0) =
+          u32x4{pack2(yl[0], yh[0]), pack2(yl[1], yh[1]), pack2(yl[2], yh[2]), pack2(yl[3], yh[3])};
+      *reinterpret_cast<u32x4*>(dst + 2 * t0 + 8) =
+          u32x4{pack2(yl[4], yh[4]), pack2(yl[5], yh[5]), pack2(yl[6], yh[6]), pack2(yl[7], yh[7])};
+    } else {
+      *reinterpret_cast<u32x4*>(dst + t0) =
+          u32x4{pack2(yl[0], yl[1]), pack2(yl[2], yl[3]), pack2(yl[4], yl[5]), pack2(yl[6], yl[7])};
+      *reinterpret_cast<u32x4*>(dst + D / 2 + t0) =
+          u32x4{pack2(yh[0], yh[1]), pack2(yh[2], yh[3]), pack2(yh[4], yh[5]), pack2(yh[6], yh[7])};
+    }
   }
 }
 
@@ -1475,19 +1551,63 @@ hipError_t decode_d(const AttnArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-int key_mode(const AttnArgs& a, bool rotate_k) { return !rotate_k ? kKeysPlain : a.local_keys ? kKeysLocal : kKeysNope; }
+int key_mode(const AttnArgs& a, bool rotate_k) {
+  return (!rotate_k ? kKeysPlain : a.local_keys ? kKeysLocal : kKeysNope) | (a.interleaved ? kInterleaved : 0);
+}
 
 template <int D>
 hipError_t prefill_dk(const AttnArgs& a, int km, hipStream_t st) {
-  return km == kKeysPlain ? prefill_d<D, kKeysPlain>(a, st)
-         : km == kKeysNope ? prefill_d<D, kKeysNope>(a, st)
-                           : prefill_d<D, kKeysLocal>(a, st);
+  switch (km) {
+    case kKeysPlain: return prefill_d<D, kKeysPlain>(a, st);
+    case kKeysNope: return prefill_d<D, kKeysNope>(a, st);
+    case kKeysLocal: return prefill_d<D, kKeysLocal>(a, st);
+    case kKeysPlain | kInterleaved: return prefill_d<D, kKeysPlain | kInterleaved>(a, st);
+    case kKeysNope | kInterleaved: return prefill_d<D, kKeysNope | kInterleaved>(a, st);
+    default: return prefill_d<D, kKeysLocal | kInterleaved>(a, st);
+  }
 }
 template <int D>
 hipError_t decode_dk(const AttnArgs& a, int km, hipStream_t st) {
-  return km == kKeysPlain ? decode_d<D, kKeysPlain>(a, st)
-         : km == kKeysNope ? decode_d<D, kKeysNope>(a, st)
-                           : decode_d<D, kKeysLocal>(a, st);
+  switch (km) {
+    case kKeysPlain: return decode_d<D, kKeysPlain>(a, st);
+    case kKeysNope: return decode_d<D, kKeysNope>(a, st);
+    case kKeysLocal: return decode_d<D, kKeysLocal>(a, st);
+    case kKeysPlain | kInterleaved: return decode_d<D, kKeysPlain | kInterleaved>(a, st);
+    case kKeysNope | kInterleaved: return decode_d<D, kKeysNope | kInterleaved>(a, st);
+    default: return decode_d<D, kKeysLocal | kInterleaved>(a, st);
+  }
+}
+template <int D>
+void shared_dk(const SharedArgs& a, dim3 grid, hipStream_t st) {
+  const int km = (a.local_keys ? kKeysLocal : kKeysNope) | (a.interleaved ? kInterleaved : 0);
+  switch (km) {
+    case kKeysNope: hipLaunchKernelGGL((decode_shared_kernel<D, kKeysNope>), grid, dim3(kThreads), 0, st, a); break;
+    case kKeysLocal: hipLaunchKernelGGL((decode_shared_kernel<D, kKeysLocal>), grid, dim3(kThreads), 0, st, a); break;
+    case kKeysNope | kInterleaved:
+      hipLaunchKernelGGL((decode_shared_kernel<D, kKeysNope | kInterleaved>), grid, dim3(kThreads), 0, st, a);
+      break;
+    default:
+      hipLaunchKernelGGL((decode_shared_kernel<D, kKeysLocal | kInterleaved>), grid, dim3(kThreads), 0, st, a);
+  }
+}
+template <int D>
+void materialize_dk(bool local, bool il, dim3 grid, hipStream_t st, const uint16_t* k_pool, const lazy_chunk_t* in,
+                    const lazy_chunk_t* plan, double log2_base, const float* inv_freq, uint16_t* k_out) {
+  if (local) {
+    if (il)
+      hipLaunchKernelGGL((materialize_rotate_kernel<D, true, true>), grid, dim3(kThreads), 0, st, k_pool, in, plan,
+                         log2_base, inv_freq, k_out);
+    else
+      hipLaunchKernelGGL((materialize_rotate_kernel<D, true, false>), grid, dim3(kThreads), 0, st, k_pool, in, plan,
+                         log2_base, inv_freq, k_out);
+  } else {
+    if (il)
+      hipLaunchKernelGGL((materialize_rotate_kernel<D, false, true>), grid, dim3(kThreads), 0, st, k_pool, in, plan,
+                         log2_base, inv_freq, k_out);
+    else
+      hipLaunchKernelGGL((materialize_rotate_kernel<D, false, false>), grid, dim3(kThreads), 0, st, k_pool, in, plan,
+                         log2_base, inv_freq, k_out);
+  }
 }
 
 }  // namespace
@@ -1525,17 +1645,10 @@ hipError_t launch_decode_shared(const SharedArgs& a, int num_items, int max_slot
   const int rows = a.batch * a.hq;
   if (num_items > 0) {
     const dim3 grid(num_items, a.hkv);
-    if (head_dim == 128) {
-      if (a.local_keys)
-        hipLaunchKernelGGL((decode_shared_kernel<128, kKeysLocal>), grid, dim3(kThreads), 0, st, a);
-      else
-        hipLaunchKernelGGL((decode_shared_kernel<128, kKeysNope>), grid, dim3(kThreads), 0, st, a);
-    } else {
-      if (a.local_keys)
-        hipLaunchKernelGGL((decode_shared_kernel<64, kKeysLocal>), grid, dim3(kThreads), 0, st, a);
-      else
-        hipLaunchKernelGGL((decode_shared_kernel<64, kKeysNope>), grid, dim3(kThreads), 0, st, a);
-    }
+    if (head_dim == 128)
+      shared_dk<128>(a, grid, st);
+    else
+      shared_dk<64>(a, grid, st);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -1553,28 +1666,20 @@ hipError_t launch_decode_shared(const SharedArgs& a, int num_items, int max_slot
 
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
                               int max_chunk_len, int hkv, int head_dim, double rope_log2_base, const float* inv_freq,
-                              bool local_keys, uint16_t* k_out, lazy_chunk_t* chunks_out, hipStream_t st) {
+                              bool local_keys, bool interleaved, uint16_t* k_out, lazy_chunk_t* chunks_out,
+                              hipStream_t st) {
   if (num_records <= 0) return hipSuccess;
   hipLaunchKernelGGL(materialize_plan_kernel, dim3(1), dim3(kThreads), 0, st, chunks, num_records, hkv, head_dim,
                      chunks_out);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || max_chunk_len <= 0) return e;
   const dim3 grid((max_chunk_len + kSub - 1) / kSub, hkv, num_records);
-  if (head_dim == 128) {
-    if (local_keys)
-      hipLaunchKernelGGL((materialize_rotate_kernel<128, true>), grid, dim3(kThreads), 0, st, k_pool, chunks,
-                         chunks_out, rope_log2_base, inv_freq, k_out);
-    else
-      hipLaunchKernelGGL((materialize_rotate_kernel<128, false>), grid, dim3(kThreads), 0, st, k_pool, chunks,
-                         chunks_out, rope_log2_base, inv_freq, k_out);
-  } else {
-    if (local_keys)
-      hipLaunchKernelGGL((materialize_rotate_kernel<64, true>), grid, dim3(kThreads), 0, st, k_pool, chunks,
-                         chunks_out, rope_log2_base, inv_freq, k_out);
-    else
-      hipLaunchKernelGGL((materialize_rotate_kernel<64, false>), grid, dim3(kThreads), 0, st, k_pool, chunks,
-                         chunks_out, rope_log2_base, inv_freq, k_out);
-  }
+  if (head_dim == 128)
+    materialize_dk<128>(local_keys, interleaved, grid, st, k_pool, chunks, chunks_out, rope_log2_base, inv_freq,
+                        k_out);
+  else
+    materialize_dk<64>(local_keys, interleaved, grid, st, k_pool, chunks, chunks_out, rope_log2_base, inv_freq,
+                       k_out);
   return hipGetLastError();
 }
 

@@ -73,6 +73,8 @@ def run_and_check(w, tag, cfg_kw=None, requests=None):
         okw["softmax_scale"] = cfg_kw["softmax_scale"]
     if cfg_kw and cfg_kw.get("key_positions") == ops.KEYS_LOCAL:
         okw["key_positions"] = "local"
+    if cfg_kw and cfg_kw.get("rope_style") == ops.ROPE_INTERLEAVED:
+        okw["pairing"] = "interleaved"
     ref_o, ref_l = oracle(w, requests=requests, **okw)
     rows = None if requests is None else rows_of(w, requests)
     assert_close(out, lse, ref_o, ref_l, rows, tag)
@@ -396,6 +398,8 @@ def run_shared_and_check(w, tag, cfg_kw=None, step=0):
     out, _ = ops.decode_shared(cfg, dw.q, dw.q_pos0, dw.pool, dw.pool, dp, lse=lse)
     torch.cuda.synchronize()
     okw = {"key_positions": "local"} if (cfg_kw or {}).get("key_positions") == ops.KEYS_LOCAL else {}
+    if (cfg_kw or {}).get("rope_style") == ops.ROPE_INTERLEAVED:
+        okw["pairing"] = "interleaved"
     ref_o, ref_l = oracle(w, **okw)
     print(f"{tag}: {plan.items.size} items for {len(w.chunks)} records, max slots {plan.max_slots}", flush=True)
     assert_close(out, lse, ref_o, ref_l, tag=tag)
@@ -476,3 +480,51 @@ def test_paged_decode_matches_oracle_per_request_and_shared(bt):
         ckw = LOCAL if local else {}
         run_and_check(w, f"paged{bt} decode {'local' if local else 'nope'}", ckw)
         run_shared_and_check(w, f"paged{bt} shared decode {'local' if local else 'nope'}", ckw)
+
+
+# --------------------------------------------------------------------------------------------------------------
+# Interleaved RoPE pairing (pairs (2t, 2t+1), Sec. 3.5): every kernel, both key conventions.
+IL = dict(rope_style=ops.ROPE_INTERLEAVED)
+
+
+@pytest.mark.parametrize("local", [False, True])
+@pytest.mark.parametrize("name", ["rag_d128_g4", "rag_d64_g2_split3", "varlen_g7"])
+def test_interleaved_prefill_matches_oracle(name, local):
+    fn, kw, ckw = PREFILL_CASES[name]
+    run_and_check(fn(**kw), f"interleaved {name} {'local' if local else 'nope'}", {**ckw, **IL, **(LOCAL if local else {})})
+
+
+@pytest.mark.parametrize("local", [False, True])
+@pytest.mark.parametrize("name", ["d128_g4", "d64_g7_split5", "d128_g20_two_head_groups"])
+def test_interleaved_decode_matches_oracle(name, local):
+    kw, ckw = DECODE_CASES[name]
+    w = W.rag_decode(**kw)
+    ck = {**ckw, **IL, **(LOCAL if local else {})}
+    run_and_check(w, f"interleaved decode {name} {'local' if local else 'nope'}", ck)
+    if name != "d128_g20_two_head_groups":  # G = 20 does not fit the shared decode's 16 columns
+        run_shared_and_check(w, f"interleaved shared decode {name} {'local' if local else 'nope'}",
+                             {k: v for k, v in ck.items() if k != "num_splits"})
+
+
+@pytest.mark.parametrize("local", [False, True])
+def test_interleaved_lazy_prefill_equals_materialize_then_attend_bitwise(local):
+    w = W.rag_prefill(seed=121, batch=3, hq=8, hkv=2, d=128, prefix_len=30, n_chunks=3, chunk_len=150,
+                      pool_chunks=5, q_len=70)
+    dw = ops.upload(w)
+    cfg = ops.config_of(w, **IL, **(LOCAL if local else {}))
+    out_l, lse_l = ops.run_lazy(dw, cfg)
+    (out_m, lse_m), (k_out, ch_out) = ops.run_materialized(dw, cfg)
+    torch.cuda.synchronize()
+    assert torch.equal(out_l.view(torch.int16), out_m.view(torch.int16))
+    assert torch.equal(lse_l, lse_m)
+    # the copy holds the interleaved-encoded keys
+    recs = ops.chunks_from_tensor(ch_out)
+    ref = O.materialize_k(w.pool, w.chunks, w.chunk_start, 2, 128, w.rope_base,
+                          key_positions="local" if local else "nope", pairing="interleaved")
+    got = k_out.float().cpu().numpy()
+    start = 0
+    for i in range(int(w.chunk_start[0]), int(w.chunk_start[1])):
+        n = int(recs[i]["len"])
+        blk = got[int(recs[i]["k_offset"]): int(recs[i]["k_offset"]) + 2 * n * 128].reshape(2, n, 128)
+        np.testing.assert_allclose(blk, ref[0][:, start:start + n], rtol=2 ** -8, atol=1e-5)
+        start += n
