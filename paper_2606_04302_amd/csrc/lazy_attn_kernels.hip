@@ -207,14 +207,17 @@ struct TileIter {
     end = c1;
     const int lane = threadIdx.x & 63;
     // Pass 1: the request's tile count.  Four blocks of 64 records are loaded at once; the first four stay in
-    // registers for pass 2.
+    // registers for pass 2.  The first block is loaded whole (one record per lane), so that the record holding the
+    // split's first tile and the one after it come from a lane instead of one more dependent load.
     int ntiles = 0, ntb[4];
+    lazy_chunk_t mine = {};
+    if (c0 + lane < c1) mine = table[c0 + lane];
     for (int k0 = c0; k0 < c1; k0 += 256) {
       int nt[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int k = k0 + 64 * u + lane;
-        nt[u] = k < c1 ? (table[k].len + TK - 1) / TK : 0;
+        nt[u] = k < c1 ? ((k0 == c0 && u == 0 ? mine.len : table[k].len) + TK - 1) / TK : 0;
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -245,8 +248,27 @@ struct TileIter {
       }
       acc = __builtin_amdgcn_readlane(incl, 63);
     }
-    cur = load_rec(recs + i);
-    if (i + 1 < end) nxt = load_rec(recs + i + 1);
+    const int f = i - c0;
+    if (f < 64) {
+      cur = lane_rec(mine, f);
+      if (i + 1 < end) nxt = f + 1 < 64 ? lane_rec(mine, f + 1) : load_rec(recs + i + 1);
+    } else {
+      cur = load_rec(recs + i);
+      if (i + 1 < end) nxt = load_rec(recs + i + 1);
+    }
+  }
+  // Lane f's record as a wave-uniform value.
+  __device__ static Rec lane_rec(const lazy_chunk_t& r, int f) {
+    Rec x;
+    x.koff = ((int64_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)r.k_offset >> 32), f) << 32) |
+             (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)r.k_offset, f);
+    x.voff = ((int64_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)r.v_offset >> 32), f) << 32) |
+             (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)r.v_offset, f);
+    x.len = __builtin_amdgcn_readlane(r.len, f);
+    x.pos = __builtin_amdgcn_readlane(r.pos_offset, f);
+    x.kst = __builtin_amdgcn_readlane(r.k_stride, f);
+    x.vst = __builtin_amdgcn_readlane(r.v_stride, f);
+    return x;
   }
   __device__ void step() {
     --left;
@@ -1366,24 +1388,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 
 // ---------------------------------------------------------------------------------------------------------------
 // Split-KV merge: per row, the splits' normalised outputs weighted by exp(lse_s - max lse), divided by the sum of
-// the weights.  A row is served by kCombineGroups x D / 8 lanes of one wave: lane (g, d8) loads 8 dims (16 bytes)
-// of the splits g, g + kCombineGroups, ...; the groups' partial sums are then added across lanes.  Every thread
-// first reads all of the row's log-sum-exps (independent loads, one round trip), so a merge over many splits costs
-// two memory round trips rather than one per split.
+// the weights.  A row is served by CG x D / 8 lanes of one wave: lane (g, d8) loads 8 dims (16 bytes) of the
+// splits g, g + CG, ... (several at once); with CG > 1 the groups' partial sums are then added across lanes.
+// Every thread first reads all of the row's log-sum-exps (independent loads, one round trip), so a merge costs
+// two memory round trips rather than one per split.  CG = 1 for a few splits, 4 for many.
 // ---------------------------------------------------------------------------------------------------------------
-constexpr int kCombineGroups = 4;
-
-template <int D>
+template <int D, int CG>
 __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __restrict__ part_o,
                                                            const float* __restrict__ part_lse, int splits, int rows,
                                                            const int32_t* __restrict__ slot_start, int hq,
                                                            uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int TPR = D / 8;
-  constexpr int LPR = TPR * kCombineGroups;  // lanes per row: 64 (D = 128) or 32 (D = 64)
+  constexpr int LPR = TPR * CG;        // lanes per row
+  constexpr int U = CG == 1 ? 4 : 2;   // splits loaded together per lane
   static_assert(LPR <= 64 && 64 % LPR == 0, "a row's lanes lie in one wave");
   const int row = blockIdx.x * (kThreads / LPR) + threadIdx.x / LPR;
   const int d8 = threadIdx.x % TPR;
-  const int grp = (threadIdx.x / TPR) % kCombineGroups;
+  const int grp = (threadIdx.x / TPR) % CG;
   // Rows past the end take part in the shuffles with no memory access (the whole wave stays converged).
   const bool live = row < rows;
   // With slot_start (shared decode), row r * hq + h of request r merges that request's own slot count.
@@ -1400,18 +1421,18 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __res
   }
   float den = 0.f, sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (live && mmax != -INFINITY) {
-    for (int s0 = grp; s0 < splits; s0 += 2 * kCombineGroups) {
-      float ls[2];
-      u32x4 v[2];
+    for (int s0 = grp; s0 < splits; s0 += U * CG) {
+      float ls[U];
+      u32x4 v[U];
 #pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int sp = s0 + e * kCombineGroups;
+      for (int e = 0; e < U; ++e) {
+        const int sp = s0 + e * CG;
         const int64_t w = (int64_t)(sp < splits ? sp : s0) * rows + row;
         ls[e] = sp < splits ? part_lse[w] : -INFINITY;
         v[e] = *reinterpret_cast<const u32x4*>(part_o + w * D + 8 * d8);
       }
 #pragma unroll
-      for (int e = 0; e < 2; ++e) {
+      for (int e = 0; e < U; ++e) {
         if (ls[e] == -INFINITY) continue;  // an empty split contributes nothing, whatever its output holds
         const float sc = expf(ls[e] - mmax);
         den += sc;
@@ -1610,20 +1631,34 @@ void materialize_dk(bool local, bool il, dim3 grid, hipStream_t st, const uint16
   }
 }
 
+template <int D, int CG>
+hipError_t combine_d(const uint16_t* part_o, const float* part_lse, int splits, int rows, const int32_t* slot_start,
+                     int hq, uint16_t* out, float* lse, hipStream_t st) {
+  constexpr int per_block = kThreads / (D / 8 * CG);
+  const dim3 grid((rows + per_block - 1) / per_block);
+  hipLaunchKernelGGL((combine_kernel<D, CG>), grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, slot_start,
+                     hq, out, lse);
+  return hipGetLastError();
+}
+
+// splits: the (largest) number of partial results per row.
+hipError_t combine_dispatch(const uint16_t* part_o, const float* part_lse, int splits, int rows,
+                            const int32_t* slot_start, int hq, int head_dim, uint16_t* out, float* lse,
+                            hipStream_t st) {
+  const bool few = splits <= 8;
+  if (head_dim == 128)
+    return few ? combine_d<128, 1>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st)
+               : combine_d<128, 4>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
+  return few ? combine_d<64, 1>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st)
+             : combine_d<64, 4>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
+}
+
 }  // namespace
 
 hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int splits, int rows, int head_dim,
                           uint16_t* out, float* lse, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  const int per_block = kThreads / (head_dim / 8 * kCombineGroups);
-  const dim3 grid((rows + per_block - 1) / per_block);
-  if (head_dim == 128)
-    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, nullptr, 1,
-                       out, lse);
-  else
-    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, nullptr, 1,
-                       out, lse);
-  return hipGetLastError();
+  return combine_dispatch(part_o, part_lse, splits, rows, nullptr, 1, head_dim, out, lse, st);
 }
 
 hipError_t launch_prefill(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t st) {
@@ -1653,15 +1688,7 @@ hipError_t launch_decode_shared(const SharedArgs& a, int num_items, int max_slot
     if (e != hipSuccess) return e;
   }
   // Ragged merge of every request's slots (a request without slots gets out = 0, lse = -inf).
-  const int per_block = kThreads / (head_dim / 8 * kCombineGroups);
-  const dim3 grid((rows + per_block - 1) / per_block);
-  if (head_dim == 128)
-    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kThreads), 0, st, a.ws_o, a.ws_lse, max_slots, rows,
-                       slot_start, a.hq, out, lse);
-  else
-    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(kThreads), 0, st, a.ws_o, a.ws_lse, max_slots, rows,
-                       slot_start, a.hq, out, lse);
-  return hipGetLastError();
+  return combine_dispatch(a.ws_o, a.ws_lse, max_slots, rows, slot_start, a.hq, head_dim, out, lse, st);
 }
 
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,
