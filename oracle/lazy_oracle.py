@@ -25,6 +25,10 @@ document's cache keeps local positions indexed from 0, and reuse at offset Delta
 whole document): the stored key j is already encoded at position j, and re-encoding it at pos_offset + j is the
 single rotation R(pos_offset) of the stored vector (the relative-rotation Fact, R(a) R(b) = R(a + b)).
 
+Score-space positions (``pairing="alibi"``, Sec. 3.5 "Score-space positional methods"): nothing is rotated; the
+scaled score of a query at m and a key at n gets the bias slope_h * (n - m) (ALiBi), with slope_h = 2^(-8 (h+1) / Hq)
+unless a table is given.  The positions come from the chunk table exactly as for RoPE.
+
 Decode is the same computation with one query token per request.  ``merge_partials`` is the plain definition of
 combining softmax statistics computed over disjoint key sets.  Parity for all of this is pinned by the CPU tests
 (textbook RoPE attention at contiguous positions, the relative-rotation Fact of Sec. 3.2, the rotate-the-query
@@ -115,10 +119,19 @@ def key_rotation_positions(kpos, offs, key_positions: str):
     raise ValueError(f"unknown key_positions {key_positions!r}")
 
 
-def attend(q_rot, k_rot, v, q_pos, k_pos, causal: bool, scale: float):
+def alibi_slopes(num_q_heads: int, slopes=None) -> np.ndarray:
+    """ALiBi slopes: 2^(-8 (h+1) / Hq) for h < Hq (the geometric sequence of the ALiBi paper for Hq a power of two),
+    or a given table verbatim."""
+    if slopes is not None:
+        return np.asarray(slopes, dtype=np.float64)
+    return np.power(2.0, -8.0 * (np.arange(num_q_heads, dtype=np.float64) + 1.0) / num_q_heads)
+
+
+def attend(q_rot, k_rot, v, q_pos, k_pos, causal: bool, scale: float, slopes=None):
     """Plain softmax attention over explicit, already rotated operands (Eqn. standard attention).
 
-    q_rot [Lq, Hq, D], k_rot / v [Hkv, L, D]; query head h uses KV head h // (Hq / Hkv).
+    q_rot [Lq, Hq, D], k_rot / v [Hkv, L, D]; query head h uses KV head h // (Hq / Hkv).  With ``slopes`` [Hq],
+    slopes[h] * (k_pos - q_pos) is added to every scaled score of head h (ALiBi).
     Returns o [Lq, Hq, D] and lse [Lq, Hq] (natural log of the sum of exp(score)), fp64.
     """
     lq, hq, d = q_rot.shape
@@ -136,6 +149,8 @@ def attend(q_rot, k_rot, v, q_pos, k_pos, causal: bool, scale: float):
     for h in range(hq):
         g = h // group
         s = (q_rot[:, h, :] @ k_rot[g].T) * scale  # [Lq, L]
+        if slopes is not None:
+            s = s + slopes[h] * (k_pos[None, :].astype(np.float64) - q_pos[:, None].astype(np.float64))
         s = np.where(visible, s, -np.inf)
         m = np.where(any_visible, s.max(axis=1), 0.0)
         w = np.exp(s - m[:, None])
@@ -153,13 +168,14 @@ def lazy_attention(q, q_start, q_pos0, pool_k, pool_v, chunks, chunk_start, num_
     """Attention of every request's query tokens over its chunk table, keys re-encoded at their positions.
 
     q [total_q, Hq, D] (NoPE queries), q_start [B+1], q_pos0 [B]: token i of request r is at q_pos0[r] + i.
-    key_positions: "nope" or "local" store convention (module docstring); pairing: "half" or "interleaved".
+    key_positions: "nope" or "local" store convention (module docstring); pairing: "half" or "interleaved" RoPE,
+    or "alibi" (no rotation; ``inv_freq`` then optionally holds the Hq slopes).
     Returns out [total_q, Hq, D] and lse [total_q, Hq] in fp64.  ``requests`` restricts the work to a subset of
     request indices (other rows stay 0 / -inf).
     """
     assert num_q_heads % num_kv_heads == 0
     scale = 1.0 / math.sqrt(head_dim) if not softmax_scale else float(softmax_scale)
-    theta = rope_frequencies(head_dim, rope_base, inv_freq)
+    theta = None if pairing == "alibi" else rope_frequencies(head_dim, rope_base, inv_freq)
     total_q = int(q_start[-1])
     out = np.zeros((total_q, num_q_heads, head_dim), dtype=np.float64)
     lse = np.full((total_q, num_q_heads), -np.inf, dtype=np.float64)
@@ -171,9 +187,13 @@ def lazy_attention(q, q_start, q_pos0, pool_k, pool_v, chunks, chunk_start, num_
         k, v, kpos, offs = request_kv(pool_k, pool_v, chunks, int(chunk_start[r]), int(chunk_start[r + 1]),
                                       num_kv_heads, head_dim, with_offsets=True)
         qpos = int(q_pos0[r]) + np.arange(b - a, dtype=np.int64)
-        k_rot = rotate(k, key_rotation_positions(kpos, offs, key_positions), theta, pairing)  # re-encoded copy
-        q_rot = rotate(np.swapaxes(np.asarray(q[a:b], dtype=np.float64), 0, 1), qpos, theta, pairing)  # [Hq, Lq, D]
-        o, l = attend(np.swapaxes(q_rot, 0, 1), k_rot, v, qpos, kpos, causal, scale)
+        if pairing == "alibi":
+            o, l = attend(np.asarray(q[a:b], dtype=np.float64), k, v, qpos, kpos, causal, scale,
+                          alibi_slopes(num_q_heads, inv_freq))
+        else:
+            k_rot = rotate(k, key_rotation_positions(kpos, offs, key_positions), theta, pairing)  # re-encoded copy
+            q_rot = rotate(np.swapaxes(np.asarray(q[a:b], dtype=np.float64), 0, 1), qpos, theta, pairing)
+            o, l = attend(np.swapaxes(q_rot, 0, 1), k_rot, v, qpos, kpos, causal, scale)
         out[a:b] = o
         lse[a:b] = l
     return out, lse

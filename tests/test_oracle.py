@@ -544,3 +544,54 @@ def test_interleaved_equals_half_split_on_permuted_queries_and_keys():
 def test_unknown_pairing_is_rejected():
     with pytest.raises(ValueError):
         O.rotate(np.zeros((1, 4)), np.zeros(1), np.ones(2), pairing="swapped")
+
+
+# ---------------------------------------------------------------------------------------------------------------
+# ALiBi (Sec. 3.5 "Score-space positional methods"): no rotation, bias slope_h * (k_pos - q_pos) on the scaled score.
+# ---------------------------------------------------------------------------------------------------------------
+def test_alibi_brute_force():
+    d = 8
+    reqs = [dict(chunks=[(5, 2), (3, 40), (2, 44)], q_len=2, q_pos0=44)]
+    w = W.custom(51, 4, 2, d, 1.0, reqs)
+    _, lse = run(w, pairing="alibi")
+    for tok in range(2):
+        m = 44 + tok
+        for h in range(4):
+            slope = 2.0 ** (-8.0 * (h + 1) / 4)
+            g = h // 2
+            scores = []
+            for rec in w.chunks:
+                for j in range(int(rec["len"])):
+                    n = int(rec["pos_offset"]) + j
+                    if n > m:
+                        continue
+                    a = int(rec["k_offset"]) + (g * int(rec["k_stride"]) + j) * d
+                    dot = sum(float(w.q[tok, h, t]) * float(w.pool[a + t]) for t in range(d))
+                    scores.append(dot / math.sqrt(d) + slope * (n - m))
+            mx = max(scores)
+            ref = mx + math.log(sum(math.exp(s - mx) for s in scores))
+            assert abs(lse[tok, h] - ref) < 1e-12
+
+
+def test_alibi_zero_slopes_is_attention_without_positions_and_shift_invariant():
+    w = W.rag_prefill(seed=52, batch=2, hq=4, hkv=2, d=16, prefix_len=5, n_chunks=3, chunk_len=11, pool_chunks=4,
+                      q_len=6)
+    w.causal = False
+    zero = np.zeros(4)
+    a, _ = run(w, pairing="alibi", inv_freq=zero)
+    # positions do not matter at all without a bias: a permuted table gives the same result
+    w2 = W.Workload(**{**w.__dict__})
+    w2.chunks = w.chunks.copy()
+    w2.chunks["pos_offset"] = w.chunks["pos_offset"][::-1].copy()
+    b, _ = run(w2, pairing="alibi", inv_freq=zero)
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+    # with the bias only relative positions matter (causal, every position moved by the same amount)
+    w.causal = True
+    c0, _ = run(w, pairing="alibi")
+    w3 = W.Workload(**{**w.__dict__})
+    w3.chunks = w.chunks.copy()
+    w3.chunks["pos_offset"] += 777
+    w3.q_pos0 = w.q_pos0 + 777
+    c1, _ = run(w3, pairing="alibi")
+    np.testing.assert_allclose(c0, c1, rtol=0, atol=1e-10)
+    assert np.allclose(O.alibi_slopes(8), [2.0 ** -(i + 1) for i in range(8)])
