@@ -368,6 +368,12 @@ def main() -> int:
                                          dp.chunk_start, wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws),
                      args.steps, args.warmup)
 
+    # ALiBi instead of RoPE (score-space positions: no rotation, one bias per score).
+    cfg_alibi = ops.config_of(wp, rope_style=ops.ALIBI)
+    alibi_ms = timed(lambda: ops.prefill(cfg_alibi, dp.q, dp.q_start, dp.q_pos0, dp.pool, dp.pool, dp.chunks,
+                                         dp.chunk_start, wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws),
+                     args.steps, args.warmup)
+
     # The same batch over a paged store (64-token blocks scattered over the pool, one record per block).
     wpp = W.paginate(wp, 64, seed=7)
     dpp = ops.upload(wpp, dev)
@@ -435,6 +441,7 @@ def main() -> int:
             "local_keys_ms": round(local_ms, 5),
             "local_keys_tflops": round(flops / (local_ms * 1e-3) / 1e12, 3),
             "paged64_ms": round(paged_ms, 5),
+            "alibi_ms": round(alibi_ms, 5),
             "materialize_ms": round(mat_ms, 5),
             "plain_attention_ms": round(plain_ms, 5),
             "materialize_then_attend_ms": round(mat_ms + plain_ms, 5),
@@ -478,6 +485,9 @@ def main() -> int:
                                                         out=outd, lse=lsed, workspace=wss), args.steps, args.warmup)
         item_keys = (plan.items["key_end"] - plan.items["key_begin"]).astype(np.int64)
         shared_read_mb = float(item_keys.sum()) * wd.num_kv_heads * wd.head_dim * 2 * 2 / 1e6
+        cfgd_alibi = ops.config_of(wd, rope_style=ops.ALIBI)
+        dalibi = timed(lambda: ops.decode(cfgd_alibi, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
+                                          wd.max_kv_len, out=outd, lse=lsed, workspace=wsd), args.steps, args.warmup)
         # The same batch over a paged store: 64-token blocks scattered over the pool, one record per block.
         wpg = W.paginate(wd, 64, seed=7)
         dpg = ops.upload(wpg, dev)
@@ -522,6 +532,7 @@ def main() -> int:
             "shared_plan_host_ms": round(plan_ms, 3),
             "shared_speedup_vs_per_request": round(dms / dshared, 3),
             "paged64_ms": round(dpaged, 5),
+            "alibi_ms": round(dalibi, 5),
             "paged64_shared_ms": round(dpaged_shared, 5),
             "materialize_ms": round(dmat, 5),
             "plain_decode_ms": round(dplain, 5),

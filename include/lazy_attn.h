@@ -77,10 +77,11 @@ typedef struct lazy_attn_params {
   int32_t causal;        /* 1: position-based causal rule; 0: every key visible */
   float rope_base;       /* theta_t = rope_base^(-2t/D); ignored if inv_freq != NULL */
   float softmax_scale;   /* 0 => 1/sqrt(D) (Eqn. standard attention) */
-  const float* inv_freq; /* optional device array of D/2 fp32 frequencies theta_t (scaled / NTK tables) */
+  const float* inv_freq; /* optional device array of D/2 fp32 frequencies theta_t (scaled / NTK tables);
+                            with LAZY_ALIBI: optional device array of Hq slopes */
   int32_t num_splits;    /* 0 => chosen by the library; otherwise the number of KV splits per request */
   int32_t key_positions; /* LAZY_KEYS_NOPE or LAZY_KEYS_LOCAL: how the chunk store holds its keys (below) */
-  int32_t rope_style;    /* LAZY_ROPE_HALF or LAZY_ROPE_INTERLEAVED: which dimensions form a rotation pair */
+  int32_t rope_style;    /* LAZY_ROPE_HALF, LAZY_ROPE_INTERLEAVED or LAZY_ALIBI: the positional method (below) */
   int32_t reserved;      /* must be 0 */
 } lazy_attn_params_t;
 
@@ -90,9 +91,16 @@ typedef struct lazy_attn_params {
  *  LAZY_ROPE_HALF        (0): pair t = dimensions (t, t + D/2), the K1/K2 halves of Sec. 3.2 "Prefilling".
  *  LAZY_ROPE_INTERLEAVED (1): pair t = dimensions (2t, 2t + 1), as in Llama's reference implementation.
  * Q, K and the materialised copy follow the style; V and the output are not affected.
+ *  LAZY_ALIBI            (2): no rotation at all; slope_h * (pos_k - pos_q) is added to every scaled score of query
+ *                             head h (ALiBi, Sec. 3.5 "Score-space positional methods"), with positions taken from
+ *                             the chunk table exactly as for RoPE.  slope_h = 2^(-8 (h+1) / Hq) unless params->inv_freq
+ *                             points to a device table of Hq fp32 slopes (that field has no other use here).  Requires
+ *                             key_positions = LAZY_KEYS_NOPE; rope_base is ignored; the materialise-then-attend
+ *                             entry points return LAZY_EUNSUPPORTED (there is nothing to re-encode).
  */
 #define LAZY_ROPE_HALF 0
 #define LAZY_ROPE_INTERLEAVED 1
+#define LAZY_ALIBI 2
 
 /*
  * Key-store conventions (params->key_positions).  Values and the causal rule are the same in both; only the

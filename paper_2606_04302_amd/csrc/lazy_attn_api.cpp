@@ -18,10 +18,12 @@ int check_params(const lazy_attn_params_t* p) {
   if (p->num_q_heads <= 0 || p->num_kv_heads <= 0 || p->num_q_heads % p->num_kv_heads != 0) return LAZY_EINVAL;
   if (p->causal != 0 && p->causal != 1) return LAZY_EINVAL;
   if (!isfinite(p->softmax_scale) || p->softmax_scale < 0.f) return LAZY_EINVAL;
-  if (!p->inv_freq && !(isfinite(p->rope_base) && p->rope_base > 0.f)) return LAZY_EINVAL;
+  if (p->rope_style != LAZY_ALIBI && !p->inv_freq && !(isfinite(p->rope_base) && p->rope_base > 0.f)) return LAZY_EINVAL;
   if (p->num_splits < 0) return LAZY_EINVAL;
   if (p->key_positions != LAZY_KEYS_NOPE && p->key_positions != LAZY_KEYS_LOCAL) return LAZY_EINVAL;
-  if (p->rope_style != LAZY_ROPE_HALF && p->rope_style != LAZY_ROPE_INTERLEAVED) return LAZY_EINVAL;
+  if (p->rope_style != LAZY_ROPE_HALF && p->rope_style != LAZY_ROPE_INTERLEAVED && p->rope_style != LAZY_ALIBI)
+    return LAZY_EINVAL;
+  if (p->rope_style == LAZY_ALIBI && p->key_positions != LAZY_KEYS_NOPE) return LAZY_EINVAL;
   if (p->reserved != 0) return LAZY_EINVAL;
   if (p->head_dim != 64 && p->head_dim != 128) return LAZY_EUNSUPPORTED;
   return LAZY_OK;
@@ -99,6 +101,7 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
                 void* out, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
   int e = check_params(p);
   if (e != LAZY_OK) return e;
+  if (!rotate_k && p->rope_style == LAZY_ALIBI) return LAZY_EUNSUPPORTED;  // no materialised copy for ALiBi
   if (batch < 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0) return LAZY_EINVAL;
   if (batch == 0 || total_q == 0) return LAZY_OK;
   if (max_q_len == 0) return LAZY_EINVAL;
@@ -134,10 +137,11 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
   a.q_tiles = q_tiles;
   a.row_blocks = prefill_row_blocks(p, max_q_len);
   a.head_groups = 1;
-  a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
+  a.rope_log2_base = p->inv_freq || p->rope_style == LAZY_ALIBI ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
   a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
+  a.alibi = p->rope_style == LAZY_ALIBI;
   return status(lazy::launch_prefill(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
 
@@ -146,6 +150,7 @@ int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const 
                int32_t max_kv_len, void* out, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
   int e = check_params(p);
   if (e != LAZY_OK) return e;
+  if (!rotate_k && p->rope_style == LAZY_ALIBI) return LAZY_EUNSUPPORTED;
   if (batch < 0 || max_kv_len < 0) return LAZY_EINVAL;
   if (batch == 0) return LAZY_OK;
   if (!q || !q_pos || !k_pool || !v_pool || !chunks || !chunk_start || !out) return LAZY_EINVAL;
@@ -180,10 +185,11 @@ int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const 
   a.q_tiles = 1;
   a.row_blocks = 1;
   a.head_groups = hg;
-  a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
+  a.rope_log2_base = p->inv_freq || p->rope_style == LAZY_ALIBI ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
   a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
+  a.alibi = p->rope_style == LAZY_ALIBI;
   return status(lazy::launch_decode(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
 
@@ -253,6 +259,7 @@ int lazy_materialize_k(const lazy_attn_params_t* params, const void* k_pool, con
                        lazy_chunk_t* chunks_out, void* stream) {
   int e = check_params(params);
   if (e != LAZY_OK) return e;
+  if (params->rope_style == LAZY_ALIBI) return LAZY_EUNSUPPORTED;
   if (num_records < 0 || max_chunk_len < 0 || total_kv < 0) return LAZY_EINVAL;
   if (num_records == 0) return LAZY_OK;
   if (!k_pool || !chunks || !chunks_out || (total_kv > 0 && !k_out)) return LAZY_EINVAL;
@@ -306,7 +313,8 @@ int lazy_attn_decode_shared(const lazy_attn_params_t* p, const void* q, const in
   a.causal = p->causal;
   a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
   a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
-  a.rope_log2_base = p->inv_freq ? 0.0 : log2((double)p->rope_base);
+  a.alibi = p->rope_style == LAZY_ALIBI;
+  a.rope_log2_base = p->inv_freq || p->rope_style == LAZY_ALIBI ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   return status(lazy::launch_decode_shared(a, num_items, max_slots, slot_start, p->head_dim,
                                            static_cast<uint16_t*>(out), lse, static_cast<hipStream_t>(stream)));

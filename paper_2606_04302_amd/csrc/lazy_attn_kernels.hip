@@ -136,6 +136,17 @@ __device__ __forceinline__ void rotate_by(float x1, float x2, float2 cs, float& 
 // materialise-then-attend baseline), NoPE keys rotated at pos_offset + j, or local-position keys (stored encoded at
 // j) rotated by the record's pos_offset.
 constexpr int kKeysPlain = 0, kKeysNope = 1, kKeysLocal = 2;
+// Score-space positions (ALiBi): keys and queries are used as stored and slope_h (k_pos - q_pos) is added to every
+// scaled score (Sec. 3.5 "Score-space positional methods").
+constexpr int kKeysAlibi = 3;
+
+// ALiBi slope of query head h: table[h], or 2^(-8 (h+1) / Hq); returned divided by the softmax scale (times
+// log2 e over scale_log2), so that adding slope' (k_pos - q_pos) to the raw dot product adds the bias to the scaled
+// score.
+__device__ __forceinline__ float alibi_slope(int h, int hq, const float* table, float scale_log2) {
+  const float sl = table ? table[h] : exp2f(-8.0f * (float)(h + 1) / (float)hq);
+  return sl * 1.4426950408889634f / scale_log2;
+}
 // Bit 2 of a kernel's key-mode argument selects the interleaved pairing (pairs (2t, 2t+1)).  Interleaved RoPE on
 // (q, k) is the half-split rotation of (P q, P k) for the permutation P: 2t -> t, 2t+1 -> t + D/2 (V unchanged), so
 // the kernels only change their Q and K loads: 16 consecutive elements are split into the pairs' first and second
@@ -403,7 +414,8 @@ template <int D, int KMI, int NT, bool CSD_REGS = false>
 struct PLoader {
   using S = TileLayout<D>;
   static constexpr int KM = keys_of(KMI);
-  static constexpr bool ROT = KM != kKeysPlain, LOCAL = KM == kKeysLocal, IL = interleaved_of(KMI);
+  static constexpr bool ROT = KM == kKeysNope || KM == kKeysLocal, LOCAL = KM == kKeysLocal,
+                        IL = interleaved_of(KMI);
   static constexpr int TPR = NT / kSub;
   static constexpr int PP = D / (2 * TPR);
   static constexpr int NV = PP / 8;
@@ -537,11 +549,12 @@ __device__ __forceinline__ void v_fragments(const uint16_t* vlane, int s2, u32x4
 // tail and position-based causal rule), the online-softmax update with lazy rescaling, and O^T += V^T P^T.
 // kb / vt: the tile's rotated K and row-major V in LDS; b0: position of the tile's first key; nvalid: keys in the
 // tile; qmin: smallest query position of the workgroup (tiles entirely at or before it need no causal mask).
-template <int D, int NT, int RB>
+// ab: per row block the ALiBi slope over the scale (only with ALIBI).
+template <int D, int NT, int RB, bool ALIBI>
 __device__ __forceinline__ void attend_tile(const uint16_t* kb, const uint16_t* vt, int lane,
                                             const bf16x8 (&qf)[RB][D / 16], f32x16 (&o)[RB][D / 32],
                                             float (&m2)[RB], float (&lsum)[RB], const int (&qpos)[RB], int b0,
-                                            int nvalid, int qmin, int causal, float c) {
+                                            int nvalid, int qmin, int causal, float c, const float (&ab)[RB]) {
   using S = TileLayout<D>;
   const int h2 = lane >> 5;
   // Transposing-read address of this lane in the V tile: row 4*(g/2) + i/4 (+ 16 per key step, + 8 for the
@@ -581,6 +594,18 @@ __device__ __forceinline__ void attend_tile(const uint16_t* kb, const uint16_t* 
     }
   }
   __builtin_amdgcn_s_setprio(0);
+  if (ALIBI) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      // key 32 blk + 8 (i / 4) + 4 h2 + i % 4: the lane's 4 h2 goes into the base, the rest is a constant
+      const float base = ab[rb] * (float)(b0 + 4 * h2 - qpos[rb]);
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          sa[rb][blk][i] = fmaf(ab[rb], (float)(32 * blk + 8 * (i >> 2) + (i & 3)), sa[rb][blk][i] + base);
+    }
+  }
   if (nvalid < kSub || (causal && b0 + kSub - 1 > qmin)) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
@@ -657,7 +682,8 @@ __global__ __launch_bounds__(NW * 64)
 __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void prefill_kernel(AttnArgs a) {
   __shared__ PrefillSmem<D, NBUF> sm;
   constexpr int KM = keys_of(KMI);
-  constexpr bool ROT = KM != kKeysPlain, LOCAL = KM == kKeysLocal, IL = interleaved_of(KMI);
+  constexpr bool ALIBI = KM == kKeysAlibi;
+  constexpr bool ROT = KM == kKeysNope || KM == kKeysLocal, LOCAL = KM == kKeysLocal, IL = interleaved_of(KMI);
   using S = TileLayout<D>;
   constexpr int NT = NW * 64;
   constexpr int BM = 32 * NW * RB;
@@ -719,13 +745,13 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
              min(kSub, it.cur.len - it.j0));
 
-  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
+  if (!ALIBI && tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
   __syncthreads();
 
   // Angle tables: per-row deltas cos/sin(delta theta_t), delta < 32 (queries and keys), and the query block bases
   // cos/sin(32 a theta_t), a = qmin / 32 .. qmax / 32.
   const int qa0 = qmin / kAngleRows, nqb = qmax / kAngleRows - qa0 + 1;
-  for (int e = tid; e < (kAngleRows + nqb) * (D / 2); e += NT) {
+  for (int e = tid; e < (ALIBI ? 0 : (kAngleRows + nqb) * (D / 2)); e += NT) {
     const int trow = e / (D / 2), t = e % (D / 2);
     float* dst = trow < kAngleRows ? sm.csd + trow * S::CSD_LD : sm.qb[trow - kAngleRows];
     const int p = trow < kAngleRows ? trow : kAngleRows * (qa0 + trow - kAngleRows);
@@ -740,7 +766,8 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     const float* qdr = sm.csd + (qpos[rb] & (kAngleRows - 1)) * S::CSD_LD;
 #pragma unroll
     for (int s = 0; s < D / 16; ++s)
-      qf[rb][s] = q_fragment_tab<D>(qraw[rb][s][0], qraw[rb][s][1], 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
+      qf[rb][s] = ALIBI ? as_bf16x8(u32x4{qraw[rb][s][0][0], qraw[rb][s][0][1], qraw[rb][s][1][0], qraw[rb][s][1][1]})
+                        : q_fragment_tab<D>(qraw[rb][s][0], qraw[rb][s][1], 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
   }
 
   f32x16 o[RB][D / 32];
@@ -753,6 +780,9 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     lsum[rb] = 0.f;
   }
   const float c = a.scale_log2;
+  float ab[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) ab[rb] = ALIBI ? alibi_slope(head[rb], a.hq, a.inv_freq, c) : 0.f;
 
   ld.load_constants(sm.csd);
 
@@ -796,7 +826,8 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
         have_ahead = ahead.seek(a.causal, qmax);
       }
     }
-    attend_tile<D, NT, RB>(sm.k[cur_buf], sm.v[cur_buf], lane, qf, o, m2, lsum, qpos, b0, nvalid, qmin, a.causal, c);
+    attend_tile<D, NT, RB, ALIBI>(sm.k[cur_buf], sm.v[cur_buf], lane, qf, o, m2, lsum, qpos, b0, nvalid, qmin,
+                                  a.causal, c, ab);
     if (NBUF == 2) {
       // Base angles two tiles ahead go to the table slot this tile used; the next tile goes to the other buffer.
       if (ROT && have_ahead)
@@ -942,10 +973,12 @@ __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, 
 // of the tile, per-row rows cd0 / cd1 of blocks 0 / 1) and S^T = K Q^T, the key mask, the online-softmax update
 // and O^T += V^T P^T.  lim: this lane's visible keys are the tile keys kk < lim (tile tail and causal rule; it may
 // differ between the lanes' columns).
-template <int D, bool ROT, bool IL>
+// ALIBI: ab = this lane's column slope over the scale, abase = ab (first key position - query position).
+template <int D, bool ROT, bool IL, bool ALIBI>
 __device__ __forceinline__ void dec_tile(const DecTile<D>& cur, uint16_t* vw, const uint16_t* vlane, const float* cb,
                                          const float* cd0, const float* cd1, const bf16x8 (&qf)[D / 32],
-                                         f32x4 (&o)[D / 16], float& m2, float& lsum, int lim, float c, int lane) {
+                                         f32x4 (&o)[D / 16], float& m2, float& lsum, int lim, float c, int lane,
+                                         float ab, float abase) {
   using S = DecodeSmem<D>;
   constexpr int SP = DecTile<D>::SP;
   const int kq = lane >> 4;
@@ -985,6 +1018,12 @@ __device__ __forceinline__ void dec_tile(const DecTile<D>& cur, uint16_t* vw, co
       sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(klo), qf[2 * s], sa[b], 0, 0, 0);
       sa[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(khi), qf[2 * s + 1], sa[b], 0, 0, 0);
     }
+  }
+  if (ALIBI) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sa[b][i] = fmaf(ab, (float)kappa(b, 4 * kq + i), sa[b][i] + abase);
   }
   if (__any(lim < kDecWaveKeys)) {
 #pragma unroll
@@ -1036,7 +1075,7 @@ template <int D, int KMI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_kernel(AttnArgs a) {
   __shared__ DecodeSmem<D> sm;
   constexpr int KM = keys_of(KMI);
-  constexpr bool IL = interleaved_of(KMI);
+  constexpr bool IL = interleaved_of(KMI), ALIBI = KM == kKeysAlibi;
   // Keys are rotated in registers only for a NoPE store; with local-position keys the query is rotated by the
   // relative offset q_pos - pos_offset whenever the record changes (Sec. 3.2 "Decoding") and the keys are used as
   // stored.
@@ -1075,7 +1114,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     dec_fetch<D, IL>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
                  min(kDecWaveKeys, it.cur.len - it.j0), lane);
 
-  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
+  if (!ALIBI && tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
   __syncthreads();
   if (ROT) {
     // Per-row constants cos/sin(delta theta_t), delta < 32: 16 per thread.
@@ -1089,7 +1128,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // Q fragments in the decode head-dimension order, rotated at the query position.  With local-position keys they
   // are built per record instead (below), from the raw query.
   bf16x8 qf[D / 32];
-  if (!LOCAL) {
+  if (ALIBI) {  // no rotation: the raw query
+#pragma unroll
+    for (int s = 0; s < SP; ++s) {
+      u32x4 ql, qh;
+      pairs_of<IL>(qraw[s][0], qraw[s][1], ql, qh);
+      qf[2 * s] = as_bf16x8(ql);
+      qf[2 * s + 1] = as_bf16x8(qh);
+    }
+  } else if (!LOCAL) {
 #pragma unroll
     for (int s = 0; s < SP; ++s) {
       float y1[8], y2[8];
@@ -1123,6 +1170,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   for (int db = 0; db < D / 16; ++db) o[db] = f32x4{};
   float m2 = -INFINITY, lsum = 0.f;
   const float c = a.scale_log2;
+  const float ab = ALIBI ? alibi_slope(head, a.hq, a.inv_freq, c) : 0.f;
 
   uint16_t* vw = sm.v[wave];
   // Transposing-read address of this lane in its V slice: row 16*(kq/2) + 4*(kq%2) + i/4 (+ 8 for the second
@@ -1169,7 +1217,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
 
     const int lim = min(nvalid, a.causal ? qpos - b0 + 1 : kDecWaveKeys);
-    dec_tile<D, ROT, IL>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane);
+    dec_tile<D, ROT, IL, ALIBI>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane, ab,
+                                ab * (float)(b0 - qpos));
     cur = nxt;
     buf ^= 1;
     have = have_next;
@@ -1236,7 +1285,7 @@ template <int D, int KMI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_shared_kernel(
     SharedArgs a) {
   constexpr int KM = keys_of(KMI);
-  constexpr bool IL = interleaved_of(KMI);
+  constexpr bool IL = interleaved_of(KMI), ALIBI = KM == kKeysAlibi;
   __shared__ DecodeSmem<D> sm;
   __shared__ float ucs[16][DecodeSmem<D>::CSB];  // per user: cos/sin(rel theta_t) at csb_idx(t)
   using S = DecodeSmem<D>;
@@ -1276,7 +1325,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     dec_fetch<D, IL>(cur, kbase + (int64_t)j0 * D, vbase + (int64_t)j0 * D, min(kDecWaveKeys, ke - j0), lane);
   }
 
-  if (tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
+  if (!ALIBI && tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
   __syncthreads();
   if (ROT) {
     for (int e = tid; e < kDecWaveKeys * (D / 2); e += kThreads) {
@@ -1287,7 +1336,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) =
           rope_cs(kb + kDecWaveKeys * tile, sm.freq[lane]);
   }
-  for (int e = tid; e < nu * (D / 2); e += kThreads) {
+  for (int e = tid; e < (ALIBI ? 0 : nu * (D / 2)); e += kThreads) {
     const int u = e / (D / 2), t = e % (D / 2);
     const lazy_shared_user_t uu = a.users[u0 + u];
     *reinterpret_cast<float2*>(&ucs[u][csb_idx<D>(t)]) = rope_cs(a.q_pos[uu.request] - uu.pos_offset, sm.freq[t]);
@@ -1301,6 +1350,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     float y1[8], y2[8];
     u32x4 ql, qh;
     pairs_of<IL>(qraw[s][0], qraw[s][1], ql, qh);
+    if (ALIBI) {  // no rotation: the raw query
+      qf[2 * s] = as_bf16x8(ql);
+      qf[2 * s + 1] = as_bf16x8(qh);
+      continue;
+    }
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float x1 = (e & 1) ? bf_hi(ql[e >> 1]) : bf_lo(ql[e >> 1]);
@@ -1318,6 +1372,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   for (int db = 0; db < D / 16; ++db) o[db] = f32x4{};
   float m2 = -INFINITY, lsum = 0.f;
   const float c = a.scale_log2;
+  const float ab = ALIBI ? alibi_slope(g * G + col % G, a.hq, a.inv_freq, c) : 0.f;
   uint16_t* vw = sm.v[wave];
   const uint16_t* vlane = vw + (16 * (kq >> 1) + 4 * (kq & 1) + ((lane & 15) >> 2)) * S::VLD + 4 * (lane & 3);
   const float* cd0 = sm.csd + kappa(0, col) * S::CSD_LD;
@@ -1334,7 +1389,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         *reinterpret_cast<float2*>(sm.csb[wave][buf ^ 1] + csb_idx<D>(lane)) = rope_cs(j1, sm.freq[lane]);
     }
     const int lim = min(nvalid, a.causal ? rel - j0 + 1 : kDecWaveKeys);
-    dec_tile<D, ROT, IL>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane);
+    dec_tile<D, ROT, IL, ALIBI>(cur, vw, vlane, sm.csb[wave][buf], cd0, cd1, qf, o, m2, lsum, lim, c, lane, ab,
+                                ab * (float)(j0 - rel));
     cur = nxt;
     buf ^= 1;
     tile = next;
@@ -1573,6 +1629,7 @@ hipError_t decode_d(const AttnArgs& a, hipStream_t st) {
 }
 
 int key_mode(const AttnArgs& a, bool rotate_k) {
+  if (a.alibi) return kKeysAlibi;
   return (!rotate_k ? kKeysPlain : a.local_keys ? kKeysLocal : kKeysNope) | (a.interleaved ? kInterleaved : 0);
 }
 
@@ -1584,6 +1641,7 @@ hipError_t prefill_dk(const AttnArgs& a, int km, hipStream_t st) {
     case kKeysLocal: return prefill_d<D, kKeysLocal>(a, st);
     case kKeysPlain | kInterleaved: return prefill_d<D, kKeysPlain | kInterleaved>(a, st);
     case kKeysNope | kInterleaved: return prefill_d<D, kKeysNope | kInterleaved>(a, st);
+    case kKeysAlibi: return prefill_d<D, kKeysAlibi>(a, st);
     default: return prefill_d<D, kKeysLocal | kInterleaved>(a, st);
   }
 }
@@ -1595,13 +1653,15 @@ hipError_t decode_dk(const AttnArgs& a, int km, hipStream_t st) {
     case kKeysLocal: return decode_d<D, kKeysLocal>(a, st);
     case kKeysPlain | kInterleaved: return decode_d<D, kKeysPlain | kInterleaved>(a, st);
     case kKeysNope | kInterleaved: return decode_d<D, kKeysNope | kInterleaved>(a, st);
+    case kKeysAlibi: return decode_d<D, kKeysAlibi>(a, st);
     default: return decode_d<D, kKeysLocal | kInterleaved>(a, st);
   }
 }
 template <int D>
 void shared_dk(const SharedArgs& a, dim3 grid, hipStream_t st) {
-  const int km = (a.local_keys ? kKeysLocal : kKeysNope) | (a.interleaved ? kInterleaved : 0);
+  const int km = a.alibi ? kKeysAlibi : (a.local_keys ? kKeysLocal : kKeysNope) | (a.interleaved ? kInterleaved : 0);
   switch (km) {
+    case kKeysAlibi: hipLaunchKernelGGL((decode_shared_kernel<D, kKeysAlibi>), grid, dim3(kThreads), 0, st, a); break;
     case kKeysNope: hipLaunchKernelGGL((decode_shared_kernel<D, kKeysNope>), grid, dim3(kThreads), 0, st, a); break;
     case kKeysLocal: hipLaunchKernelGGL((decode_shared_kernel<D, kKeysLocal>), grid, dim3(kThreads), 0, st, a); break;
     case kKeysNope | kInterleaved:

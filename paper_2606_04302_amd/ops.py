@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblazyattn
 
 LAZY_OK, LAZY_EINVAL, LAZY_EUNSUPPORTED, LAZY_EWORKSPACE, LAZY_EHIP, LAZY_EDATA = 0, -1, -2, -3, -4, -5
 KEYS_NOPE, KEYS_LOCAL = 0, 1  # key-store conventions (lazy_attn_params_t.key_positions)
-ROPE_HALF, ROPE_INTERLEAVED = 0, 1  # rotation pairs (lazy_attn_params_t.rope_style)
+ROPE_HALF, ROPE_INTERLEAVED, ALIBI = 0, 1, 2  # positional method (lazy_attn_params_t.rope_style)
 
 _c_i32, _c_i64, _c_f32, _c_p, _c_sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -123,7 +123,7 @@ class Config:
     inv_freq: torch.Tensor | None = None  # device fp32 [D/2]
     num_splits: int = 0
     key_positions: int = 0  # KEYS_NOPE or KEYS_LOCAL
-    rope_style: int = 0  # ROPE_HALF or ROPE_INTERLEAVED
+    rope_style: int = 0  # ROPE_HALF, ROPE_INTERLEAVED or ALIBI (then inv_freq optionally holds the Hq slopes)
 
     def c(self) -> LazyAttnParams:
         return LazyAttnParams(self.num_q_heads, self.num_kv_heads, self.head_dim, int(bool(self.causal)),

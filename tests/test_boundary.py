@@ -143,7 +143,13 @@ def test_scalar_argument_errors_return_before_any_launch(ops):
     assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, -1, 0)) == ops.LAZY_EINVAL         # splits
     assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 7)) == ops.LAZY_EINVAL          # key convention
     assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, -1)) == ops.LAZY_EINVAL
-    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0, 2)) == ops.LAZY_EINVAL      # rotation pairs
+    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0, 3)) == ops.LAZY_EINVAL      # positional method
+    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 1, 2)) == ops.LAZY_EINVAL      # ALiBi with local keys
+    L = ops.lib()
+    alibi = P(8, 2, 128, 1, 0.0, 0.0, None, 0, 0, 2)                                  # rope_base unused
+    assert L.lazy_plain_attn_prefill(ctypes.byref(alibi), *([1] * 7), 1, 1, 1, 1, 1, None, None, 0,
+                                     None) == ops.LAZY_EUNSUPPORTED
+    assert L.lazy_materialize_k(ctypes.byref(alibi), 1, 1, 1, 1, 1, 1, 1, None) == ops.LAZY_EUNSUPPORTED
     assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0, 0, 1)) == ops.LAZY_EINVAL   # reserved
     assert prefill(good, batch=-1) == ops.LAZY_EINVAL
     assert prefill(good, batch=0) == ops.LAZY_OK                                       # nothing to do

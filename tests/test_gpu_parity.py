@@ -75,6 +75,8 @@ def run_and_check(w, tag, cfg_kw=None, requests=None):
         okw["key_positions"] = "local"
     if cfg_kw and cfg_kw.get("rope_style") == ops.ROPE_INTERLEAVED:
         okw["pairing"] = "interleaved"
+    if cfg_kw and cfg_kw.get("rope_style") == ops.ALIBI:
+        okw["pairing"] = "alibi"
     ref_o, ref_l = oracle(w, requests=requests, **okw)
     rows = None if requests is None else rows_of(w, requests)
     assert_close(out, lse, ref_o, ref_l, rows, tag)
@@ -400,6 +402,8 @@ def run_shared_and_check(w, tag, cfg_kw=None, step=0):
     okw = {"key_positions": "local"} if (cfg_kw or {}).get("key_positions") == ops.KEYS_LOCAL else {}
     if (cfg_kw or {}).get("rope_style") == ops.ROPE_INTERLEAVED:
         okw["pairing"] = "interleaved"
+    if (cfg_kw or {}).get("rope_style") == ops.ALIBI:
+        okw["pairing"] = "alibi"
     ref_o, ref_l = oracle(w, **okw)
     print(f"{tag}: {plan.items.size} items for {len(w.chunks)} records, max slots {plan.max_slots}", flush=True)
     assert_close(out, lse, ref_o, ref_l, tag=tag)
@@ -528,3 +532,38 @@ def test_interleaved_lazy_prefill_equals_materialize_then_attend_bitwise(local):
         blk = got[int(recs[i]["k_offset"]): int(recs[i]["k_offset"]) + 2 * n * 128].reshape(2, n, 128)
         np.testing.assert_allclose(blk, ref[0][:, start:start + n], rtol=2 ** -8, atol=1e-5)
         start += n
+
+
+# --------------------------------------------------------------------------------------------------------------
+# ALiBi (score-space positions, Sec. 3.5): no rotation, slope_h (k_pos - q_pos) added to the scaled scores.
+ALIBI = dict(rope_style=ops.ALIBI)
+
+
+@pytest.mark.parametrize("name", ["rag_d128_g4", "rag_d64_g2_split3", "varlen_g7"])
+def test_alibi_prefill_matches_oracle(name):
+    fn, kw, ckw = PREFILL_CASES[name]
+    run_and_check(fn(**kw), f"alibi {name}", {**ckw, **ALIBI})
+
+
+@pytest.mark.parametrize("name", ["d128_g4", "d64_g7_split5", "d128_g20_two_head_groups"])
+def test_alibi_decode_matches_oracle(name):
+    kw, ckw = DECODE_CASES[name]
+    w = W.rag_decode(**kw)
+    run_and_check(w, f"alibi decode {name}", {**ckw, **ALIBI})
+    if name != "d128_g20_two_head_groups":
+        run_shared_and_check(w, f"alibi shared decode {name}", ALIBI)
+
+
+def test_alibi_slope_table_and_non_causal():
+    w = W.rag_prefill(seed=131, batch=2, hq=8, hkv=2, d=128, prefix_len=20, n_chunks=2, chunk_len=90,
+                      pool_chunks=3, q_len=30)
+    slopes = np.linspace(0.5, 0.01, 8).astype(np.float32)
+    dw = ops.upload(w)
+    cfg = ops.config_of(w, rope_style=ops.ALIBI, inv_freq=torch.tensor(slopes, device="cuda"))
+    for causal in (True, False):
+        w.causal = causal
+        cfg.causal = causal
+        out, lse = ops.run_lazy(dw, cfg)
+        torch.cuda.synchronize()
+        ref_o, ref_l = oracle(w, pairing="alibi", inv_freq=slopes.astype(np.float64))
+        assert_close(out, lse, ref_o, ref_l, tag=f"alibi table causal={causal}")
