@@ -261,6 +261,26 @@ LAZY_API size_t lazy_attn_decode_shared_workspace_size(const lazy_attn_params_t*
                                                        int32_t max_slots);
 
 /*
+ * Position-agnostic chunk pool (host only).  A serving system keeps reusable chunks in a device KV region of
+ * `capacity_slots` equal-size slots; this LRU directory maps a 64-bit id to its slot.  With position-free storage
+ * the id is the document alone, so one slot serves every request at every offset (Sec. 2 "Hit-ratio impact under
+ * limited cache capacity": a position-aware cache spends its capacity on positional variants; such a cache would
+ * key by (document, position)).  The caller fills a slot on a miss and builds lazy_chunk_t records from slot
+ * numbers.  Not thread-safe: one owner per pool.
+ *   lazy_pool_create      NULL on a non-positive capacity or allocation failure.
+ *   lazy_pool_acquire     *hit = 1 and the slot of `key` (now most recent), or *hit = 0 and a slot for it: a free
+ *                         one, else the least recently used one, whose key is reported (*evicted = 1).
+ *   lazy_pool_stats       counters since creation; any output may be NULL.
+ */
+typedef struct lazy_pool lazy_pool_t;
+LAZY_API lazy_pool_t* lazy_pool_create(int32_t capacity_slots);
+LAZY_API void lazy_pool_destroy(lazy_pool_t* pool);
+LAZY_API int lazy_pool_acquire(lazy_pool_t* pool, uint64_t key, int32_t* slot, int32_t* hit, uint64_t* evicted_key,
+                               int32_t* evicted);
+LAZY_API int lazy_pool_stats(const lazy_pool_t* pool, int64_t* lookups, int64_t* hits, int64_t* evictions,
+                             int32_t* resident);
+
+/*
  * Host-side check of the table contents against the layout contract, on HOST copies of the tables (CPU only, no
  * device access).  k_pool_elems / v_pool_elems are the pool sizes in elements.  Returns LAZY_OK or LAZY_EDATA and
  * writes the offending record / request index and a reason to *bad_index / reason (either may be NULL).

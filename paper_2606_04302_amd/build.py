@@ -35,6 +35,7 @@ SOURCES = [
     ("lazy_attn_api.cpp", "hip"),
     ("lazy_attn_validate.cpp", "host"),
     ("lazy_attn_plan.cpp", "host"),
+    ("lazy_attn_pool.cpp", "host"),
 ]
 
 

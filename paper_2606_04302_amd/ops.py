@@ -73,6 +73,12 @@ SIGNATURES = {
     "lazy_attn_decode_shared": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_p,
                                          _c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_sz, _c_p]),
     "lazy_attn_decode_shared_workspace_size": (_c_sz, [ctypes.POINTER(LazyAttnParams), _c_i32, _c_i32]),
+    "lazy_pool_create": (_c_p, [_c_i32]),
+    "lazy_pool_destroy": (None, [_c_p]),
+    "lazy_pool_acquire": (_c_i32, [_c_p, ctypes.c_uint64, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32),
+                                   ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(_c_i32)]),
+    "lazy_pool_stats": (_c_i32, [_c_p, ctypes.POINTER(_c_i64), ctypes.POINTER(_c_i64), ctypes.POINTER(_c_i64),
+                                 ctypes.POINTER(_c_i32)]),
     "lazy_attn_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "lazy_attn_version": (ctypes.c_int, []),
 }
