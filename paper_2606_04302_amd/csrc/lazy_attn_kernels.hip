@@ -3,8 +3,11 @@
 // The chunk store holds K and V without positional encoding (Sec. 3.1 "Deferred encoding").  Every kernel that
 // reads K rotates it on the way from HBM into LDS, at position pos_offset + j of the chunk in the current request
 // (Sec. 3.2 "Prefilling": one rotation of the two half-dimensions per key, never "back to zero then forward").
+// Variants selected per kernel instance: keys stored at local positions (one rotation by the record offset in
+// prefill, the query rotated per record in decode), interleaved pairs (2t, 2t+1), and ALiBi (no rotation, a bias
+// on every score); see the key-mode constants below.
 //
-// Data path of one key tile (64 keys per sub-tile, shared by the four waves of a workgroup):
+// Data path of one key tile (64 keys per sub-tile, shared by the waves of a workgroup):
 //   global K rows (bf16, natural layout) --16 B loads--> registers --fp32 rotation--> bf16 --> LDS K tile
 //   global V rows --16 B loads--> registers --> LDS V tile (row-major), read back transposed by ds_read_b64_tr_b16
 // The rotation is done once per workgroup and tile (not once per wave), which matters on gfx950 where the bf16
@@ -13,9 +16,9 @@
 //
 // Rotation angles are stateless (Appendix "Long-Context Scalability and Numerical Stability": absolute indices,
 // no recurrence).  theta_t is held in revolutions per position in fp64; for a tile whose row 0 sits at position b
-// the workgroup computes cos/sin(b theta_t) once per t, and each loader thread keeps cos/sin(delta theta_t) for
-// its fixed row delta in a private slice of LDS (written once per workgroup); the angle of row b + delta follows by
-// one angle addition.
+// the workgroup computes cos/sin(b theta_t) once per t (per 32-row half), and each loader thread keeps
+// cos/sin(delta theta_t) for its fixed row delta (from a 32-row LDS table written once per workgroup, held in
+// registers by the eight-wave kernel); the angle of row b + delta follows by one angle addition.
 //
 // Operand layouts (verified for v_mfma_f32_32x32x16_bf16 and v_mfma_f32_16x16x32_bf16):
 //   32x32x16: A[i][k] in lane i%32 ... k = 8*(lane/32)+e; B[k][j] in lane j%32, k = 8*(lane/32)+e;
@@ -371,12 +374,13 @@ __device__ __forceinline__ const uint16_t* v_ptr(const uint16_t* pool, const Rec
 }
 
 // ---------------------------------------------------------------------------------------------------------------
-// Prefill: workgroup = (row tile of 128*RB packed query rows, KV head, request x split).  Packed row = token * G + g
-// (the G query heads sharing one KV head, Sec. 3.5).  Four waves; each wave owns RB blocks of 32 rows, one row per
-// lane pair (lane, lane+32).  With RB = 2 every K / V fragment read from LDS feeds two MFMAs and the K rotation of
-// a tile is shared by 256 rows.  NBUF = 2 double-buffers the LDS tiles (one barrier per tile, the next tile's
-// global loads in flight during the current tile's MFMAs); NBUF = 1 keeps the LDS small enough for two
-// workgroups per CU.
+// Prefill: workgroup = (row tile of 32*NW*RB packed query rows, KV head, request x split).  Packed row =
+// token * G + g (the G query heads sharing one KV head, Sec. 3.5).  NW waves; each wave owns RB blocks of 32 rows,
+// one row per lane pair (lane, lane+32).  The launch uses eight waves x one block (256 rows, the K rotation of a
+// tile shared by all of them) or four waves x one block (128 rows); RB = 2 (every K / V fragment read from LDS
+// feeding two MFMAs) exists as a compile-time option but needs more registers than a wave has.  NBUF = 2
+// double-buffers the LDS tiles (one barrier per tile, the next tile's global loads in flight during the current
+// tile's MFMAs); NBUF = 1 keeps the LDS small enough for two workgroups per CU.
 // ---------------------------------------------------------------------------------------------------------------
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).  Remapping the linear workgroup id
 // so that consecutive logical ids share an XCD puts the row tiles that read the same keys onto one L2.
