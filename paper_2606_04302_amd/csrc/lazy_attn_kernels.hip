@@ -311,21 +311,24 @@ struct TileIter {
 // with cos/sin of each part from rope_cs and one angle addition (rotate_pair).
 constexpr int kAngleRows = 32;
 
-// LDS layout constants of a 64-key prefill tile.  Bank-conflict notes (4-byte banks; a 16-byte access pattern is
-// conflict free when every group of 8 consecutive lanes covers distinct 16-byte bank groups):
-//  - K tile rows are D + 8 elements apart (a 4-bank shift per row); the 16-byte blocks of a row are permuted by
-//    kblk_t() so that the loader threads writing one row do not collide.
-//  - The V tile is row-major (key, dimension) with rows D + 16 elements apart: the 16-byte writes of a row are
-//    contiguous, and the transposing reads (ds_read_b64_tr_b16: 16 lanes read 4 rows x 32 bytes) hit 4 disjoint
-//    8-bank groups.
-//  - cos/sin tables interleave (c, s) and leave 8 floats of gap per loader quarter and a 4-float row tail so that
-//    the 16-byte reads of the threads of one 8-lane group hit distinct banks.
+// LDS layout constants of a 64-key prefill tile.  Bank-conflict notes: gfx950 LDS has 64 banks of 4 bytes and
+// serves a 16-byte read for 16 lanes per pass (8-byte reads: 32 lanes per pass; writes: 8 lanes per pass, half
+// the read rate); a pattern is conflict free when the lanes of one pass that read distinct addresses cover
+// distinct banks.
+//  - K tile rows are D + 8 elements apart (a 4-bank shift per row, so 16 consecutive rows of one 16-byte column
+//    tile the 64 banks); the 16-byte blocks of a row are permuted by kblk_t().
+//  - The V tile is row-major (key, dimension) with rows D + 32 elements apart (a 16-bank shift per row): the
+//    transposing reads (ds_read_b64_tr_b16: 32 lanes read 4 rows x 64 bytes per pass) hit 4 disjoint 16-bank
+//    groups.  With rows D + 16 apart they conflict two ways.
+//  - cos/sin rows interleave (c, s) with a 4-float gap after every 32 pairs (cs_idx), and the per-row table has a
+//    row stride of 8 (mod 64) floats for D = 128 and 4 for D = 64: the 16-byte reads of the loader threads of
+//    one pass (4 or 8 threads per key row) hit distinct banks.
 template <int D>
 struct TileLayout {
-  static constexpr int KLD = D + kPad;       // K tile: [64][KLD], head dimension in virtual order
-  static constexpr int VLD = D + 16;         // V tile: [64][VLD], natural layout
-  static constexpr int CSW = D + 32;         // floats per cos/sin row: (c, s) of pair t at 2t + 8 * (t / (D / 8))
-  static constexpr int CSD_LD = CSW + 4;     // row stride of the per-row table (4 banks of shift per row)
+  static constexpr int KLD = D + kPad;                    // K tile: [64][KLD], head dimension in virtual order
+  static constexpr int VLD = D + 32;                      // V tile: [64][VLD], natural layout
+  static constexpr int CSW = D + 4 * ((D / 2 - 1) / 32);  // floats per cos/sin row: (c, s) of pair t at cs_idx(t)
+  static constexpr int CSD_LD = CSW + 4;                  // row stride of the per-row table
 };
 
 // Transposing LDS read (gfx950 ds_read_b64_tr_b16).  Within each group of 16 lanes, lane i supplies the address
@@ -338,7 +341,7 @@ __device__ __forceinline__ u32x2 tr_read(const uint16_t* p) {
   return __builtin_bit_cast(u32x2, v);
 }
 template <int D>
-__device__ __forceinline__ int cs_idx(int t) { return 2 * t + 8 * (t / (D / 8)); }
+__device__ __forceinline__ int cs_idx(int t) { return 2 * t + 4 * (t / 32); }
 
 // Four query pairs (t0..t0+3 with their partners t0+D/2..) of one query row (raw bf16: lo = elements t0..t0+3,
 // hi = t0+D/2..t0+D/2+3), rotated at position p, as one 8-element
