@@ -82,7 +82,7 @@ typedef struct lazy_attn_params {
   int32_t num_splits;    /* 0 => chosen by the library; otherwise the number of KV splits per request */
   int32_t key_positions; /* LAZY_KEYS_NOPE or LAZY_KEYS_LOCAL: how the chunk store holds its keys (below) */
   int32_t rope_style;    /* LAZY_ROPE_HALF, LAZY_ROPE_INTERLEAVED or LAZY_ALIBI: the positional method (below) */
-  int32_t reserved;      /* must be 0 */
+  int32_t q_prerotated;  /* 0: q is position-free and the kernels rotate it; 1: q arrives already rotated (below) */
 } lazy_attn_params_t;
 
 /*
@@ -97,6 +97,13 @@ typedef struct lazy_attn_params {
  *                             points to a device table of Hq fp32 slopes (that field has no other use here).  Requires
  *                             key_positions = LAZY_KEYS_NOPE; rope_base is ignored; the materialise-then-attend
  *                             entry points return LAZY_EUNSUPPORTED (there is nothing to re-encode).
+ *
+ * Pre-rotated queries (params->q_prerotated = 1): q holds R(q_pos) q in the chosen pairing, as the paper's prefill
+ * assumes (Sec. 3.2, tiling figure panel (b): only keys are rotated inside the kernel).  The kernels then leave the
+ * query as it is where they would rotate it at q_pos, and where they rotate it by a relative offset q_pos - pos_offset
+ * (decode over local-position keys, the chunk-major shared decode) they rotate it by -pos_offset instead, since
+ * R(q_pos - pos_offset) q = R(-pos_offset) R(q_pos) q.  Positions still come from q_pos0 / q_pos for the causal rule.
+ * No effect with LAZY_ALIBI (nothing is rotated).  Any value other than 0 or 1 is LAZY_EINVAL.
  */
 #define LAZY_ROPE_HALF 0
 #define LAZY_ROPE_INTERLEAVED 1

@@ -24,7 +24,7 @@ int check_params(const lazy_attn_params_t* p) {
   if (p->rope_style != LAZY_ROPE_HALF && p->rope_style != LAZY_ROPE_INTERLEAVED && p->rope_style != LAZY_ALIBI)
     return LAZY_EINVAL;
   if (p->rope_style == LAZY_ALIBI && p->key_positions != LAZY_KEYS_NOPE) return LAZY_EINVAL;
-  if (p->reserved != 0) return LAZY_EINVAL;
+  if (p->q_prerotated != 0 && p->q_prerotated != 1) return LAZY_EINVAL;
   if (p->head_dim != 64 && p->head_dim != 128) return LAZY_EUNSUPPORTED;
   return LAZY_OK;
 }
@@ -142,6 +142,7 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
   a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
   a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
   a.alibi = p->rope_style == LAZY_ALIBI;
+  a.q_prerot = p->q_prerotated && p->rope_style != LAZY_ALIBI;
   return status(lazy::launch_prefill(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
 
@@ -190,6 +191,7 @@ int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const 
   a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
   a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
   a.alibi = p->rope_style == LAZY_ALIBI;
+  a.q_prerot = p->q_prerotated && p->rope_style != LAZY_ALIBI;
   return status(lazy::launch_decode(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
 
@@ -314,6 +316,7 @@ int lazy_attn_decode_shared(const lazy_attn_params_t* p, const void* q, const in
   a.local_keys = p->key_positions == LAZY_KEYS_LOCAL;
   a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
   a.alibi = p->rope_style == LAZY_ALIBI;
+  a.q_prerot = p->q_prerotated && p->rope_style != LAZY_ALIBI;
   a.rope_log2_base = p->inv_freq || p->rope_style == LAZY_ALIBI ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   return status(lazy::launch_decode_shared(a, num_items, max_slots, slot_start, p->head_dim,

@@ -35,6 +35,7 @@ struct AttnArgs {
   int32_t local_keys;         // 1: the store holds keys encoded at local positions (LAZY_KEYS_LOCAL)
   int32_t interleaved;        // 1: RoPE pairs (2t, 2t+1) (LAZY_ROPE_INTERLEAVED)
   int32_t alibi;              // 1: no rotation, ALiBi bias (LAZY_ALIBI); inv_freq then holds optional slopes
+  int32_t q_prerot;           // 1: q arrives rotated at its own positions (rotations use -pos_offset / none)
   double rope_log2_base;      // log2(rope_base), computed on the host (unused with inv_freq)
   float scale_log2;           // softmax scale * log2(e)
 };
@@ -58,6 +59,7 @@ struct SharedArgs {
   int32_t local_keys;
   int32_t interleaved;
   int32_t alibi;
+  int32_t q_prerot;
   double rope_log2_base;
   float scale_log2;
 };

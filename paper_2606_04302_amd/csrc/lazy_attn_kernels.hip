@@ -773,8 +773,9 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     const float* qdr = sm.csd + (qpos[rb] & (kAngleRows - 1)) * S::CSD_LD;
 #pragma unroll
     for (int s = 0; s < D / 16; ++s)
-      qf[rb][s] = ALIBI ? as_bf16x8(u32x4{qraw[rb][s][0][0], qraw[rb][s][0][1], qraw[rb][s][1][0], qraw[rb][s][1][1]})
-                        : q_fragment_tab<D>(qraw[rb][s][0], qraw[rb][s][1], 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
+      qf[rb][s] = (ALIBI || a.q_prerot)
+                      ? as_bf16x8(u32x4{qraw[rb][s][0][0], qraw[rb][s][0][1], qraw[rb][s][1][0], qraw[rb][s][1][1]})
+                      : q_fragment_tab<D>(qraw[rb][s][0], qraw[rb][s][1], 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
   }
 
   f32x16 o[RB][D / 32];
@@ -1135,7 +1136,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // Q fragments in the decode head-dimension order, rotated at the query position.  With local-position keys they
   // are built per record instead (below), from the raw query.
   bf16x8 qf[D / 32];
-  if (ALIBI) {  // no rotation: the raw query
+  if (ALIBI || (!LOCAL && a.q_prerot)) {  // no rotation: the query as given
 #pragma unroll
     for (int s = 0; s < SP; ++s) {
       u32x4 ql, qh;
@@ -1194,7 +1195,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       // angle row to this wave's table (same-wave LDS ordering: written here, read just below).
       qdelta = it.cur.pos;
       if (lane < D / 2)
-        *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(qpos - qdelta, sm.freq[lane]);
+        *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) =
+            rope_cs((a.q_prerot ? 0 : qpos) - qdelta, sm.freq[lane]);
 #pragma unroll
       for (int s = 0; s < SP; ++s) {
         float y1[8], y2[8];
@@ -1346,7 +1348,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   for (int e = tid; e < (ALIBI ? 0 : nu * (D / 2)); e += kThreads) {
     const int u = e / (D / 2), t = e % (D / 2);
     const lazy_shared_user_t uu = a.users[u0 + u];
-    *reinterpret_cast<float2*>(&ucs[u][csb_idx<D>(t)]) = rope_cs(a.q_pos[uu.request] - uu.pos_offset, sm.freq[t]);
+    *reinterpret_cast<float2*>(&ucs[u][csb_idx<D>(t)]) =
+        rope_cs((a.q_prerot ? 0 : a.q_pos[uu.request]) - uu.pos_offset, sm.freq[t]);
   }
   __syncthreads();
 

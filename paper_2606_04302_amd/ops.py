@@ -35,7 +35,7 @@ class LazyAttnParams(ctypes.Structure):
         ("num_splits", _c_i32),
         ("key_positions", _c_i32),
         ("rope_style", _c_i32),
-        ("reserved", _c_i32),
+        ("q_prerotated", _c_i32),
     ]
 
 
@@ -130,12 +130,13 @@ class Config:
     num_splits: int = 0
     key_positions: int = 0  # KEYS_NOPE or KEYS_LOCAL
     rope_style: int = 0  # ROPE_HALF, ROPE_INTERLEAVED or ALIBI (then inv_freq optionally holds the Hq slopes)
+    q_prerotated: bool = False  # q already holds R(q_pos) q
 
     def c(self) -> LazyAttnParams:
         return LazyAttnParams(self.num_q_heads, self.num_kv_heads, self.head_dim, int(bool(self.causal)),
                               float(self.rope_base), float(self.softmax_scale),
                               None if self.inv_freq is None else self.inv_freq.data_ptr(), int(self.num_splits),
-                              int(self.key_positions), int(self.rope_style), 0)
+                              int(self.key_positions), int(self.rope_style), int(bool(self.q_prerotated)))
 
 
 def config_of(w: Workload, **kw) -> Config:

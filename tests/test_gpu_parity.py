@@ -4,6 +4,7 @@ Tolerance (bf16 outputs): max |gpu - oracle| <= 2e-2 and mean |gpu - oracle| <= 
 and -inf exactly where the oracle has no visible key.  Lazy (in-kernel rotation) and materialise-then-attend
 compute the same rotated bf16 keys, so they must agree bit for bit.
 """
+import dataclasses
 import math
 
 import numpy as np
@@ -567,3 +568,82 @@ def test_alibi_slope_table_and_non_causal():
         torch.cuda.synchronize()
         ref_o, ref_l = oracle(w, pairing="alibi", inv_freq=slopes.astype(np.float64))
         assert_close(out, lse, ref_o, ref_l, tag=f"alibi table causal={causal}")
+
+
+# --------------------------------------------------------------------------------------------------------------
+# Pre-rotated queries (q_prerotated = 1): the caller passes R(q_pos) q, as the paper's prefill assumes.  The queries
+# are rotated here by the oracle (fp64) and rounded to bf16; the result must match the oracle on the raw queries.
+def with_prerotated_q(w, pairing="half"):
+    if w.kind == "decode":
+        pos = np.asarray(w.q_pos0, dtype=np.int64)
+    else:
+        pos = np.concatenate([int(w.q_pos0[r]) + np.arange(int(w.q_start[r + 1] - w.q_start[r]))
+                              for r in range(w.batch)]).astype(np.int64)
+    theta = O.rope_frequencies(w.head_dim, w.rope_base)
+    q = O.rotate(np.transpose(w.q, (1, 0, 2)), pos, theta, pairing)  # [Hq, n, D]
+    w2 = dataclasses.replace(w, q=W.bf16_round(np.transpose(q, (1, 0, 2)).astype(np.float32)))
+    return w2
+
+
+def check_prerotated(w, tag, ckw, shared=False):
+    okw = {}
+    if ckw.get("key_positions") == ops.KEYS_LOCAL:
+        okw["key_positions"] = "local"
+    pairing = "interleaved" if ckw.get("rope_style") == ops.ROPE_INTERLEAVED else "half"
+    if pairing == "interleaved":
+        okw["pairing"] = "interleaved"
+    w2 = with_prerotated_q(w, pairing)
+    cfg = ops.config_of(w, q_prerotated=True, **ckw)
+    dw = ops.upload(w2)
+    if shared:
+        dp = ops.upload_plan(ops.shared_decode_plan(cfg, w.chunks, w.chunk_start, 0))
+        lse = torch.empty((w.batch, w.num_q_heads), dtype=torch.float32, device="cuda")
+        out, _ = ops.decode_shared(cfg, dw.q, dw.q_pos0, dw.pool, dw.pool, dp, lse=lse)
+    else:
+        out, lse = ops.run_lazy(dw, cfg)
+    torch.cuda.synchronize()
+    ref_o, ref_l = oracle(w, **okw)
+    assert_close(out, lse, ref_o, ref_l, tag=tag)
+    # the flag really changes the computation: without it the pre-rotated queries are rotated twice
+    if not shared:
+        out2, _ = ops.run_lazy(dw, ops.config_of(w, **ckw))
+        torch.cuda.synchronize()
+        assert np.abs(out2.float().cpu().numpy() - ref_o).max() > 5 * MAX_ABS, tag
+
+
+PREROT = {"nope": {}, "local": LOCAL, "interleaved": IL, "interleaved_local": {**IL, **LOCAL}}
+
+
+@pytest.mark.parametrize("mode", list(PREROT))
+@pytest.mark.parametrize("name", ["rag_d128_g4", "rag_d64_g2_split3", "varlen_g7"])
+def test_prerotated_queries_prefill(name, mode):
+    fn, kw, ckw = PREFILL_CASES[name]
+    check_prerotated(fn(**kw), f"prerotated prefill {name} {mode}", {**ckw, **PREROT[mode]})
+
+
+@pytest.mark.parametrize("mode", list(PREROT))
+@pytest.mark.parametrize("name", ["d128_g4", "d64_g7_split5", "d128_g20_two_head_groups"])
+def test_prerotated_queries_decode(name, mode):
+    kw, ckw = DECODE_CASES[name]
+    check_prerotated(W.rag_decode(**kw), f"prerotated decode {name} {mode}", {**ckw, **PREROT[mode]})
+
+
+@pytest.mark.parametrize("mode", ["nope", "local", "interleaved"])
+@pytest.mark.parametrize("name", ["g4_shared", "g7_d64_split37"])
+def test_prerotated_queries_shared_decode(name, mode):
+    kw, _, _ = SHARED_CASES[name]
+    check_prerotated(W.rag_decode(**kw), f"prerotated shared {name} {mode}", PREROT[mode], shared=True)
+
+
+def test_prerotated_queries_plain_attention_equals_lazy_bitwise():
+    """The materialise-then-attend baseline honours the flag too: bit-identical to the lazy kernel."""
+    fn, kw, ckw = PREFILL_CASES["rag_d128_g4"]
+    w = fn(**kw)
+    w2 = with_prerotated_q(w)
+    cfg = ops.config_of(w, q_prerotated=True, **ckw)
+    dw = ops.upload(w2)
+    lazy, lse_l = ops.run_lazy(dw, cfg)
+    (plain, lse_m), _ = ops.run_materialized(dw, cfg)
+    torch.cuda.synchronize()
+    assert torch.equal(lazy.view(torch.int16), plain.view(torch.int16))
+    assert torch.equal(lse_l, lse_m)
