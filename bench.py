@@ -97,6 +97,26 @@ def timed_graph(fn, reps: int, inner: int = 20):
     return start.elapsed_time(end) / (reps * inner)
 
 
+def timed_cold(fn, reps: int, scrub_mib: int = 512):
+    """Average ms per call with cold caches: before every call a 512 MiB buffer (twice the 256 MB MALL, far more than
+    the L2s) is overwritten, then the call alone is bracketed by HIP events.  The scrub is queued ahead of the call,
+    so the events time the call and not its launch."""
+    import torch
+
+    scrub = torch.empty(scrub_mib << 20, dtype=torch.uint8, device="cuda")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    fn()
+    for i in range(reps):
+        scrub.fill_(i & 0x7F)
+        ev[i][0].record()
+        fn()
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in ev) / reps
+    del scrub
+    return ms
+
+
 def cpu_baseline(w, flops_per_pass: float, budget_s: float = 12.0):
     """The fp64 oracle on the host cores, whole passes over the same batch until ``budget_s`` has elapsed."""
     from oracle import lazy_oracle as O
@@ -259,6 +279,81 @@ def other_configs(dev, steps: int, warmup: int, log):
     }
     del k_mat, dw, ws, wsd
 
+    # ---- overhead-ablation shape: one request, 5 x 4096-token chunks + a 64-token query ----
+    log("e3_overhead workload: generating")
+    w = W.rag_prefill(seed=5, batch=1, prefix_len=0, n_chunks=5, chunk_len=4096, pool_chunks=5, q_len=64)
+    dw = ops.upload(w, dev)
+    cfg = dw.cfg
+    flops = A.useful_flops(w)
+    ws = torch.empty(max(16, ops.prefill_workspace_size(cfg, w.batch, w.total_q, w.max_q_len, w.max_kv_len)),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty_like(dw.q)
+
+    def e3(c, plain=False):
+        return lambda: ops.prefill(c, dw.q, dw.q_start, dw.q_pos0, dw.pool, dw.pool, dw.chunks, dw.chunk_start,
+                                   w.max_q_len, w.max_kv_len, out=out, workspace=ws, plain=plain)
+
+    log("e3_overhead: timing")
+    ms = timed(e3(cfg), steps, warmup)
+    norot = timed(e3(cfg, True), steps, warmup)
+    local = timed(e3(ops.config_of(w, key_positions=ops.KEYS_LOCAL)), steps, warmup)
+    mat_fn, k_mat, ch_mat = materialized(w, dw, w.chunks)
+    mat_ms = timed(mat_fn, max(5, steps // 5), 2)
+    res["e3_overhead"] = {
+        "workload": "one request, 32/8 heads, head_dim 128, base 5e5, 5 x 4096-token chunks + 64-token causal query "
+                    "(the shape of the paper's rotation-overhead ablation)",
+        "prefill_ms": round(ms, 5),
+        "tflops": round(flops / (ms * 1e-3) / 1e12, 3),
+        "no_rotation_ms": round(norot, 5),
+        "rotation_overhead": round(ms / norot - 1.0, 4),
+        "local_keys_ms": round(local, 5),
+        "local_keys_overhead": round(local / norot - 1.0, 4),
+        "materialize_ms": round(mat_ms, 5),
+        "speedup_vs_materialize": round((mat_ms + norot) / ms, 3),
+    }
+    del dw, ws, k_mat
+
+    # ---- icl decode with private pools: every request owns its 128 exemplars (no sharing, 537 MB) ----
+    log("icl_private workload: generating")
+    w = W.icl_prefill(seed=3, private=True)
+    dw = ops.upload(w, dev)
+    cfg = dw.cfg
+    own = [int(w.chunk_start[r + 1]) - 1 for r in range(w.batch)]
+    tables, pbytes, max_kv = [], 0, 0
+    hq, hkv, d = w.num_q_heads, w.num_kv_heads, w.head_dim
+    for s in range(int(w.meta["decode_steps"])):
+        ch = w.chunks.copy()
+        qpos = np.empty(w.batch, dtype=np.int32)
+        for r, i in enumerate(own):
+            ch[i]["len"] = int(w.q_lens[r]) + s + 1
+            qpos[r] = int(ch[i]["pos_offset"]) + int(ch[i]["len"]) - 1
+        lens = [int(ch[int(w.chunk_start[r]):int(w.chunk_start[r + 1])]["len"].astype(np.int64).sum())
+                for r in range(w.batch)]
+        max_kv = max(max_kv, max(lens))
+        pbytes += sum(lens) * hkv * d * 2 * 2 + 2 * w.batch * hq * d * 2
+        tables.append((ops.chunks_tensor(ch, dev), torch.from_numpy(qpos).to(dev)))
+    rng = np.random.default_rng(33)
+    qd = ops.bf16_tensor(W.bf16_round(rng.standard_normal((w.batch, hq, d), dtype=np.float32)), dev)
+    outd = torch.empty_like(qd)
+    wsd = torch.empty(max(16, ops.decode_workspace_size(cfg, w.batch, max_kv)), dtype=torch.uint8, device=dev)
+
+    def decode_private():
+        for ch, qp in tables:
+            ops.decode(cfg, qd, qp, dw.pool, dw.pool, ch, dw.chunk_start, max_kv, out=outd, workspace=wsd)
+
+    log("icl_private: timing 128 decode steps")
+    pms = timed(decode_private, max(3, steps // 40), 2)
+    res["icl_private"] = {
+        "workload": "icl with private pools: batch 4, 32/8 heads, head_dim 128, each request its own 128 x "
+                    "256-token exemplars, 256-token query at 32,768, then 128 decode steps",
+        "decode_128_steps_ms": round(pms, 4),
+        "decode_ms_per_step": round(pms / len(tables), 5),
+        "decode_logical_hbm_gbps": round(pbytes / (pms * 1e-3) / 1e9, 1),
+        "decode_logical_hbm_frac": round(pbytes / (pms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "unique_kv_mb": round(A.unique_kv_bytes(w) / 1e6, 1),
+    }
+    del dw, wsd, tables
+
     # ---- varlen_rag prefill ----
     log("varlen_rag workload: generating")
     w = W.varlen_rag(seed=4)
@@ -356,6 +451,9 @@ def main() -> int:
         combine_ms = timed_graph(lambda: ops.combine(part_o, part_lse, out=out2, lse=lse2), max(20, args.steps // 4))
     kernel_ms = ms - combine_ms
 
+    # Cold caches: every launch after a 512 MiB scrub, so the store comes from HBM and not from the MALL / L2s.
+    cold_ms = timed_cold(prefill, max(10, args.steps // 10))
+
     # No-rotation diagnostic: the same kernel with K rotation compiled out, over the unrotated store.
     norot_ms = timed(lambda: ops.prefill(cfg, dp.q, dp.q_start, dp.q_pos0, dp.pool, dp.pool, dp.chunks,
                                          dp.chunk_start, wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws,
@@ -436,6 +534,8 @@ def main() -> int:
             "kernel_ms": round(kernel_ms, 5),
             "combine_ms": round(combine_ms, 5),
             "logical_hbm_gbps": round(alg_bytes / (ms * 1e-3) / 1e9, 1),
+            "cold_cache_ms": round(cold_ms, 5),
+            "cold_cache_tflops": round(flops / (cold_ms * 1e-3) / 1e12, 3),
             "no_rotation_ms": round(norot_ms, 5),
             "rotation_overhead": round(ms / norot_ms - 1.0, 4),
             "local_keys_ms": round(local_ms, 5),
@@ -466,6 +566,9 @@ def main() -> int:
         log("decode: timing")
         dms = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
                                        wd.max_kv_len, out=outd, lse=lsed, workspace=wsd), args.steps, args.warmup)
+        dcold = timed_cold(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
+                                              wd.max_kv_len, out=outd, lse=lsed, workspace=wsd),
+                           max(10, args.steps // 20))
         dnorot = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
                                           wd.max_kv_len, out=outd, lse=lsed, workspace=wsd, plain=True),
                        args.steps, args.warmup)
@@ -517,6 +620,7 @@ def main() -> int:
             "ms": round(dms, 5),
             "logical_hbm_gbps": round(gbps, 1),
             "hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
+            "cold_cache_ms": round(dcold, 5),
             "logical_mb": round(dbytes / 1e6, 1),
             "unique_kv_mb": round(A.unique_kv_bytes(wd) / 1e6, 1),
             "splits": int(wsd_bytes // (wd.batch * wd.num_q_heads * (2 * wd.head_dim + 4))) if wsd_bytes else 1,

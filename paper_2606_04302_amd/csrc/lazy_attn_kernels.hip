@@ -766,16 +766,17 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   }
   __syncthreads();
 
+  // Pre-rotated queries take the angle row of position 0 (cos 1, sin 0) for both parts, which leaves them exactly
+  // as given without a second code path.
   bf16x8 qf[RB][D / 16];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const float* qbr = sm.qb[qpos[rb] / kAngleRows - qa0];
-    const float* qdr = sm.csd + (qpos[rb] & (kAngleRows - 1)) * S::CSD_LD;
+    const float* qbr = a.q_prerot ? sm.csd : sm.qb[qpos[rb] / kAngleRows - qa0];
+    const float* qdr = sm.csd + (a.q_prerot ? 0 : qpos[rb] & (kAngleRows - 1)) * S::CSD_LD;
 #pragma unroll
     for (int s = 0; s < D / 16; ++s)
-      qf[rb][s] = (ALIBI || a.q_prerot)
-                      ? as_bf16x8(u32x4{qraw[rb][s][0][0], qraw[rb][s][0][1], qraw[rb][s][1][0], qraw[rb][s][1][1]})
-                      : q_fragment_tab<D>(qraw[rb][s][0], qraw[rb][s][1], 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
+      qf[rb][s] = ALIBI ? as_bf16x8(u32x4{qraw[rb][s][0][0], qraw[rb][s][0][1], qraw[rb][s][1][0], qraw[rb][s][1][1]})
+                        : q_fragment_tab<D>(qraw[rb][s][0], qraw[rb][s][1], 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
   }
 
   f32x16 o[RB][D / 32];
@@ -1136,7 +1137,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // Q fragments in the decode head-dimension order, rotated at the query position.  With local-position keys they
   // are built per record instead (below), from the raw query.
   bf16x8 qf[D / 32];
-  if (ALIBI || (!LOCAL && a.q_prerot)) {  // no rotation: the query as given
+  if (ALIBI) {  // no rotation: the raw query
 #pragma unroll
     for (int s = 0; s < SP; ++s) {
       u32x4 ql, qh;
@@ -1155,7 +1156,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       for (int e = 0; e < 8; ++e) {
         const float x1 = (e & 1) ? bf_hi(ql[e >> 1]) : bf_lo(ql[e >> 1]);
         const float x2 = (e & 1) ? bf_hi(qh[e >> 1]) : bf_lo(qh[e >> 1]);
-        rotate_q_pair(x1, x2, qpos, sm.freq[t0 + e], y1[e], y2[e]);
+        rotate_q_pair(x1, x2, a.q_prerot ? 0 : qpos, sm.freq[t0 + e], y1[e], y2[e]);  // position 0: identity
       }
       qf[2 * s] =
           as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y1[4], y1[5]), pack2(y1[6], y1[7])});

@@ -271,15 +271,17 @@ def rag_decode(seed: int = 2, batch: int = 64, hq: int = 32, hkv: int = 8, d: in
 
 def icl_prefill(seed: int = 3, batch: int = 4, hq: int = 32, hkv: int = 8, d: int = 128, base: float = 5.0e5,
                 n_chunks: int = 128, chunk_len: int = 256, q_len: int = 256, decode_steps: int = 128,
-                slack_fill=None) -> Workload:
+                slack_fill=None, private: bool = False) -> Workload:
     """Many-shot in-context learning: one shared pool of exemplar chunks, an independent permutation of all of
     them per request (contiguous), then a causal query; the query's own K/V chunk has room for
-    ``decode_steps`` more tokens."""
+    ``decode_steps`` more tokens.  ``private``: every request gets its own pool of exemplars instead (no sharing)."""
     rng = np.random.default_rng(seed)
     store = _Store(hkv, d)
     pool_ids = [store.add(chunk_len) for _ in range(n_chunks)]
     uses, q_pos0 = [], []
-    for _ in range(batch):
+    for r in range(batch):
+        if private and r > 0:
+            pool_ids = [store.add(chunk_len) for _ in range(n_chunks)]
         perm = rng.permutation(n_chunks)
         uses.append([(pool_ids[int(c)], chunk_len, i * chunk_len) for i, c in enumerate(perm)])
         q_pos0.append(n_chunks * chunk_len)
