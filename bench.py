@@ -586,8 +586,7 @@ def main() -> int:
                                                   lse=lsed, workspace=wss), args.steps, args.warmup)
         dshared_local = timed(lambda: ops.decode_shared(cfgd_local, dd.q, dd.q_pos0, dd.pool, dd.pool, dplan,
                                                         out=outd, lse=lsed, workspace=wss), args.steps, args.warmup)
-        item_keys = (plan.items["key_end"] - plan.items["key_begin"]).astype(np.int64)
-        shared_read_mb = float(item_keys.sum()) * wd.num_kv_heads * wd.head_dim * 2 * 2 / 1e6
+        shared_read_mb = float(plan.read_keys()) * wd.num_kv_heads * wd.head_dim * 2 * 2 / 1e6
         cfgd_alibi = ops.config_of(wd, rope_style=ops.ALIBI)
         dalibi = timed(lambda: ops.decode(cfgd_alibi, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
                                           wd.max_kv_len, out=outd, lse=lsed, workspace=wsd), args.steps, args.warmup)

@@ -210,58 +210,80 @@ LAZY_API int lazy_plain_attn_decode(const lazy_attn_params_t* params, const void
  * Chunk-major shared decode.  Position-free storage lets one stored chunk serve several requests of a batch at
  * different offsets (the problem statement at the start of Sec. 3).  In decode, where reading K/V dominates
  * (Sec. 3.2 "Decoding"), such a batch can read every shared chunk once per step for all of its users instead of
- * once per user.  A work item is one key range of one stored chunk together with up to floor(16 / G) of its users
- * (G = num_q_heads / num_kv_heads <= 16); its workgroups (one per KV head) read the range once and score it
- * against every (user, query head) pair.  User u's query is rotated by the relative offset q_pos[r_u] - pos_offset_u
- * (the query-side rotation of Sec. 3.2 "Decoding"); keys are used at their local index j: as stored for a
- * local-position store, rotated by R(j) for a NoPE store, since (R(q_pos) q).(R(pos_offset + j) k) =
- * (R(q_pos - pos_offset) q).(R(j) k) (the relative-rotation Fact of Sec. 3.2).  The causal rule is applied per
- * user (key j visible iff pos_offset_u + j <= q_pos[r_u]).  Every (user, item) writes one partial result into its
- * request's slot; the request's slots are then merged as in lazy_attn_combine.
+ * once per user.  A work item is a run of stored keys (one or more ranges of records, read back to back) together
+ * with up to floor(16 / G) of its users (G = num_q_heads / num_kv_heads <= 16); its workgroups (one per KV head) read
+ * the run once and score it against every (user, query head) pair.  Key j of the run (j counted from 0 over its
+ * ranges) sits at position pos_offset_u + j in user u's request.  User u's query is rotated by the relative offset
+ * q_pos[r_u] - pos_offset_u (the query-side rotation of Sec. 3.2 "Decoding") and keys are rotated by R(j) for a
+ * NoPE store, since (R(q_pos) q).(R(pos_offset + j) k) = (R(q_pos - pos_offset) q).(R(j) k) (the relative-rotation
+ * Fact of Sec. 3.2).  A local-position store holds keys already encoded at their index in the record, so its items
+ * are single ranges, the keys are used as stored and the query is rotated by the record's own offset,
+ * q_pos[r_u] - (pos_offset_u - key_begin).  The causal rule is applied per user (key j visible iff
+ * pos_offset_u + j <= q_pos[r_u]).  Every (user, item) writes one partial result into its request's slot; the
+ * request's slots are then merged as in lazy_attn_combine.
  */
-typedef struct lazy_shared_item {
-  int64_t k_offset;   /* the stored chunk, as in lazy_chunk_t */
+typedef struct lazy_shared_range {
+  int64_t k_offset;   /* a stored record, as in lazy_chunk_t */
   int64_t v_offset;
   int32_t k_stride;
   int32_t v_stride;
-  int32_t key_begin;  /* this item covers the chunk's keys key_begin .. key_end - 1 */
+  int32_t key_begin;  /* this range is the record's keys key_begin .. key_end - 1 */
   int32_t key_end;
-  int32_t user_begin; /* its users are users[user_begin .. user_begin + num_users - 1] */
-  int32_t num_users;  /* 1 .. floor(16 / G) */
-} lazy_shared_item_t; /* 40 bytes */
+} lazy_shared_range_t; /* 32 bytes */
+
+typedef struct lazy_shared_item {
+  int32_t range_begin; /* its keys: ranges[range_begin .. range_begin + num_ranges - 1], back to back */
+  int32_t num_ranges;  /* 1 .. LAZY_SHARED_MAX_RANGES */
+  int32_t range_keys;  /* keys in every range but the last, a multiple of 32 when num_ranges > 1; the last range
+                          has 1 .. range_keys keys */
+  int32_t user_begin;  /* its users are users[user_begin .. user_begin + num_users - 1] */
+  int32_t num_users;   /* 1 .. floor(16 / G) */
+  int32_t reserved;    /* 0 */
+} lazy_shared_item_t; /* 24 bytes */
+
+#define LAZY_SHARED_MAX_RANGES 64
 
 typedef struct lazy_shared_user {
   int32_t request;    /* the request: row block of q, q_pos and out */
-  int32_t pos_offset; /* the chunk's offset in that request */
+  int32_t pos_offset; /* position of the item's first key in that request */
   int32_t slot;       /* partial-result slot within the request, 0 .. (slot_start[r+1] - slot_start[r]) - 1 */
   int32_t reserved;   /* 0 */
 } lazy_shared_user_t; /* 16 bytes */
 
 /*
- * Host planner (CPU only, on HOST copies of the decode tables): groups the records that read the same stored keys
- * (same k_offset, v_offset, k_stride, v_stride) and cuts each record into pieces of at most max_keys_per_item keys
- * (0 = 1024).  Each piece of each record is one (user, item) pair; pieces of one stored range with the same bounds
- * share items.  Items are ordered by key count, longest first.  Writes *num_items items, *num_users users and
- * slot_start[batch+1] (prefix sums of the slots per request).  Returns LAZY_EINVAL if a capacity is too small (the
- * counts needed are still written), LAZY_EUNSUPPORTED if G > 16, LAZY_EDATA for a negative length.
+ * Host planner (CPU only, on HOST copies of the decode tables).
+ *  1. Groups the records that read the same stored keys (same k_offset, v_offset, k_stride, v_stride) and cuts
+ *     each record into pieces of at most max_keys_per_item keys (0 = 1024); pieces with the same bounds share a
+ *     group, whose users are the (request, piece) pairs.
+ *  2. With a NoPE store (key_positions = LAZY_KEYS_NOPE, any rope_style), chains groups into runs: group B follows
+ *     group A when both cover whole records, A holds a multiple of 32 keys, B at most as many, and every user of A
+ *     continues, in its own table, with the next record in B at the next position (so a chunk held as a sequence of
+ *     blocks, e.g. a paged store, is read as one run).  A run stops at max_keys_per_item keys or
+ *     LAZY_SHARED_MAX_RANGES ranges.
+ *  3. Every (request, run) gets one slot; runs become items of up to floor(16 / G) users, longest first.
+ * Writes *num_items items, *num_ranges ranges, *num_users users and slot_start[batch+1] (prefix sums of the slots
+ * per request).  Returns LAZY_EINVAL if a capacity is too small (the counts needed are still written),
+ * LAZY_EUNSUPPORTED if G > 16, LAZY_EDATA for a negative length.
  */
 LAZY_API int lazy_shared_decode_plan(const lazy_attn_params_t* params, const lazy_chunk_t* chunks,
                                      const int32_t* chunk_start, int32_t batch, int32_t max_keys_per_item,
-                                     lazy_shared_item_t* items, int32_t item_capacity, lazy_shared_user_t* users,
-                                     int32_t user_capacity, int32_t* num_items, int32_t* num_users,
+                                     lazy_shared_item_t* items, int32_t item_capacity, lazy_shared_range_t* ranges,
+                                     int32_t range_capacity, lazy_shared_user_t* users, int32_t user_capacity,
+                                     int32_t* num_items, int32_t* num_ranges, int32_t* num_users,
                                      int32_t* slot_start);
 
 /*
  * Shared decode over a plan (all arrays in device memory): q [batch][Hq][D] bf16, q_pos [batch] int32, items /
- * users / slot_start as written by lazy_shared_decode_plan, max_slots >= the largest slot count of a request.
- * out [batch][Hq][D] bf16 and lse [batch][Hq] (or NULL) as for lazy_attn_decode.  workspace: at least
+ * ranges / users / slot_start as written by lazy_shared_decode_plan, max_slots >= the largest slot count of a
+ * request.  out [batch][Hq][D] bf16 and lse [batch][Hq] (or NULL) as for lazy_attn_decode.  workspace: at least
  * lazy_attn_decode_shared_workspace_size(params, batch, max_slots) bytes, holding the partial results
  * [max_slots][batch * Hq] (bf16 outputs, then fp32 log-sum-exps).  Requests with no slot get out = 0, lse = -inf.
  */
 LAZY_API int lazy_attn_decode_shared(const lazy_attn_params_t* params, const void* q, const int32_t* q_pos,
                                      const void* k_pool, const void* v_pool, const lazy_shared_item_t* items,
-                                     int32_t num_items, const lazy_shared_user_t* users, const int32_t* slot_start,
-                                     int32_t batch, int32_t max_slots, void* out, float* lse, void* workspace,
+                                     int32_t num_items, const lazy_shared_range_t* ranges,
+                                     const lazy_shared_user_t* users, const int32_t* slot_start, int32_t batch,
+                                     int32_t max_slots, void* out, float* lse, void* workspace,
                                      size_t workspace_bytes, void* stream);
 
 LAZY_API size_t lazy_attn_decode_shared_workspace_size(const lazy_attn_params_t* params, int32_t batch,

@@ -283,15 +283,15 @@ size_t lazy_attn_decode_shared_workspace_size(const lazy_attn_params_t* params, 
 
 int lazy_attn_decode_shared(const lazy_attn_params_t* p, const void* q, const int32_t* q_pos, const void* k_pool,
                             const void* v_pool, const lazy_shared_item_t* items, int32_t num_items,
-                            const lazy_shared_user_t* users, const int32_t* slot_start, int32_t batch,
-                            int32_t max_slots, void* out, float* lse, void* workspace, size_t workspace_bytes,
-                            void* stream) {
+                            const lazy_shared_range_t* ranges, const lazy_shared_user_t* users,
+                            const int32_t* slot_start, int32_t batch, int32_t max_slots, void* out, float* lse,
+                            void* workspace, size_t workspace_bytes, void* stream) {
   int e = check_params(p);
   if (e != LAZY_OK) return e;
   if (p->num_q_heads / p->num_kv_heads > 16) return LAZY_EUNSUPPORTED;
   if (batch < 0 || num_items < 0 || max_slots < 0 || (num_items > 0 && max_slots == 0)) return LAZY_EINVAL;
   if (batch == 0) return LAZY_OK;
-  if (!q || !q_pos || !k_pool || !v_pool || !slot_start || !out || (num_items > 0 && (!items || !users)))
+  if (!q || !q_pos || !k_pool || !v_pool || !slot_start || !out || (num_items > 0 && (!items || !ranges || !users)))
     return LAZY_EINVAL;
   if (p->num_kv_heads > 65535) return LAZY_EUNSUPPORTED;
   const size_t need = lazy_attn_decode_shared_workspace_size(p, batch, max_slots);
@@ -302,6 +302,7 @@ int lazy_attn_decode_shared(const lazy_attn_params_t* p, const void* q, const in
   a.k_pool = static_cast<const uint16_t*>(k_pool);
   a.v_pool = static_cast<const uint16_t*>(v_pool);
   a.items = items;
+  a.ranges = ranges;
   a.users = users;
   const int64_t rows = (int64_t)batch * p->num_q_heads;
   a.ws_o = need ? static_cast<uint16_t*>(workspace) : nullptr;

@@ -47,6 +47,7 @@ struct SharedArgs {
   const uint16_t* k_pool;
   const uint16_t* v_pool;
   const lazy_shared_item_t* items;   // [num_items]
+  const lazy_shared_range_t* ranges; // key ranges of the items' runs
   const lazy_shared_user_t* users;
   uint16_t* ws_o;                    // [max_slots][batch*hq][D] bf16 partial outputs
   float* ws_lse;                     // [max_slots][batch*hq]

@@ -1283,14 +1283,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 }
 
 // ---------------------------------------------------------------------------------------------------------------
-// Chunk-major shared decode: workgroup = (work item, KV head).  A work item is one key range of one stored chunk
-// with up to 16 / G users (requests that hold the chunk, each at its own offset); MFMA column c is the pair
-// (user c / G, query head c % G).  The range's K / V are read once for all users.  Column c's query is rotated by
-// its user's relative offset rel = q_pos - pos_offset, and the keys are used at their local index j (as stored for
-// a local-position store, rotated by R(j) in registers for a NoPE store); key j is visible to the column iff
-// j <= rel under the causal rule.  Waves take the range's 32-key tiles w, w + 4, ... with the next tile in flight,
-// as in decode_kernel, and every (user, item) writes one partial result into its request's slot.
+// Chunk-major shared decode: workgroup = (work item, KV head).  A work item is a run of stored keys (one or more
+// ranges of records, read back to back) with up to 16 / G users (requests that read the run, each at its own
+// offset); MFMA column c is the pair (user c / G, query head c % G).  The run's K / V are read once for all users.
+// Key j of the run is at position pos_offset + j for a user.  Column c's query is rotated by its user's relative
+// offset rel = q_pos - pos_offset and the keys are rotated by R(j) in registers (NoPE store), or used as stored
+// with the query rotated by the record's own offset (local-position store, single-range items); key j is visible to
+// the column iff j <= rel under the causal rule.  Waves take the run's 32-key tiles w, w + 4, ... with the next tile
+// in flight, as in decode_kernel; tile t lies in range 32 t / range_keys (every range but the last holds a multiple
+// of 32 keys).  Every (user, item) writes one partial result into its request's slot.
 // ---------------------------------------------------------------------------------------------------------------
+// K / V address of key j (within the run) of KV head g: range j / rk of the run, whose ranges are staged in LDS.
+__device__ __forceinline__ void run_key(const lazy_shared_range_t* rg, int nr, int rk, int g, int j, int d,
+                                        int64_t& koff, int64_t& voff) {
+  const int r = nr == 1 ? 0 : j / rk;
+  const int jr = j - r * rk + rg[r].key_begin;
+  koff = rg[r].k_offset + ((int64_t)g * rg[r].k_stride + jr) * d;
+  voff = rg[r].v_offset + ((int64_t)g * rg[r].v_stride + jr) * d;
+}
+
 template <int D, int KMI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_shared_kernel(
     SharedArgs a) {
@@ -1302,11 +1313,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   constexpr int SP = DecTile<D>::SP;
   constexpr bool ROT = KM == kKeysNope;
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  __shared__ lazy_shared_range_t srg[LAZY_SHARED_MAX_RANGES];
   const cptr<lazy_shared_item_t> item = as_const(a.items) + blockIdx.x;
   const int g = blockIdx.y;
-  const int64_t koff = item->k_offset, voff = item->v_offset;
-  const int kst = item->k_stride, vst = item->v_stride, kb = item->key_begin, ke = item->key_end;
+  const int rb = item->range_begin, nr = item->num_ranges, rk = item->range_keys;
   const int u0 = item->user_begin, nu = item->num_users;
+  const cptr<lazy_shared_range_t> rgs = as_const(a.ranges) + rb;
+  const int nk = (nr - 1) * rk + (rgs[nr - 1].key_end - rgs[nr - 1].key_begin);  // keys of the run
+  if (tid < nr) srg[tid] = a.ranges[rb + tid];
   const int G = a.group;
   const int col = lane & 15, kq = lane >> 4;
   const int cu = col / G;
@@ -1325,14 +1339,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       if (cvalid) dec_k_pairs<D, IL>(qrow, s, kq, qraw[s][0], qraw[s][1]);
     }
   }
-  const uint16_t* kbase = a.k_pool + koff + (int64_t)g * kst * D;
-  const uint16_t* vbase = a.v_pool + voff + (int64_t)g * vst * D;
-  const int ntiles = (ke - kb + kDecWaveKeys - 1) / kDecWaveKeys;
+  const int ntiles = (nk + kDecWaveKeys - 1) / kDecWaveKeys;
   int tile = wave;
   DecTile<D> cur, nxt;
-  if (tile < ntiles) {
-    const int j0 = kb + kDecWaveKeys * tile;
-    dec_fetch<D, IL>(cur, kbase + (int64_t)j0 * D, vbase + (int64_t)j0 * D, min(kDecWaveKeys, ke - j0), lane);
+  if (tile < ntiles) {  // the first tile straight from the range table (the LDS copy is not ready yet)
+    const int j0 = kDecWaveKeys * tile;
+    const int r = nr == 1 ? 0 : j0 / rk;
+    const int jr = j0 - r * rk + rgs[r].key_begin;
+    dec_fetch<D, IL>(cur, a.k_pool + rgs[r].k_offset + ((int64_t)g * rgs[r].k_stride + jr) * D,
+                     a.v_pool + rgs[r].v_offset + ((int64_t)g * rgs[r].v_stride + jr) * D,
+                     min(kDecWaveKeys, nk - j0), lane);
   }
 
   if (!ALIBI && tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
@@ -1343,14 +1359,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       *reinterpret_cast<float2*>(sm.csd + dr * S::CSD_LD + 2 * t) = rope_cs(dr, sm.freq[t]);
     }
     if (tile < ntiles && lane < D / 2)
-      *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) =
-          rope_cs(kb + kDecWaveKeys * tile, sm.freq[lane]);
+      *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(kDecWaveKeys * tile, sm.freq[lane]);
   }
+  // Per user: the query rotation q_pos - pos_offset (NoPE), or by the record's own offset (local-position keys are
+  // encoded at their index in the record, key_begin for the run's first key).
+  const int qrot_shift = KM == kKeysLocal ? rgs[0].key_begin : 0;
   for (int e = tid; e < (ALIBI ? 0 : nu * (D / 2)); e += kThreads) {
     const int u = e / (D / 2), t = e % (D / 2);
     const lazy_shared_user_t uu = a.users[u0 + u];
     *reinterpret_cast<float2*>(&ucs[u][csb_idx<D>(t)]) =
-        rope_cs((a.q_prerot ? 0 : a.q_pos[uu.request]) - uu.pos_offset, sm.freq[t]);
+        rope_cs((a.q_prerot ? 0 : a.q_pos[uu.request]) - uu.pos_offset + qrot_shift, sm.freq[t]);
   }
   __syncthreads();
 
@@ -1390,12 +1408,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const float* cd1 = sm.csd + kappa(1, col) * S::CSD_LD;
   int buf = 0;
   while (tile < ntiles) {
-    const int j0 = kb + kDecWaveKeys * tile;
-    const int nvalid = min(kDecWaveKeys, ke - j0);
+    const int j0 = kDecWaveKeys * tile;
+    const int nvalid = min(kDecWaveKeys, nk - j0);
     const int next = tile + 4;
     if (next < ntiles) {
-      const int j1 = kb + kDecWaveKeys * next;
-      dec_fetch<D, IL>(nxt, kbase + (int64_t)j1 * D, vbase + (int64_t)j1 * D, min(kDecWaveKeys, ke - j1), lane);
+      const int j1 = kDecWaveKeys * next;
+      int64_t k1, v1;
+      run_key(srg, nr, rk, g, j1, D, k1, v1);
+      dec_fetch<D, IL>(nxt, a.k_pool + k1, a.v_pool + v1, min(kDecWaveKeys, nk - j1), lane);
       if (ROT && lane < D / 2)
         *reinterpret_cast<float2*>(sm.csb[wave][buf ^ 1] + csb_idx<D>(lane)) = rope_cs(j1, sm.freq[lane]);
     }

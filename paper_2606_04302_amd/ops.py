@@ -47,10 +47,13 @@ class LazyChunk(ctypes.Structure):
 assert ctypes.sizeof(LazyChunk) == CHUNK_DTYPE.itemsize == 32
 
 # Plan records of the chunk-major shared decode (lazy_shared_item_t, lazy_shared_user_t).
-ITEM_DTYPE = np.dtype([("k_offset", "<i8"), ("v_offset", "<i8"), ("k_stride", "<i4"), ("v_stride", "<i4"),
-                       ("key_begin", "<i4"), ("key_end", "<i4"), ("user_begin", "<i4"), ("num_users", "<i4")])
+RANGE_DTYPE = np.dtype([("k_offset", "<i8"), ("v_offset", "<i8"), ("k_stride", "<i4"), ("v_stride", "<i4"),
+                        ("key_begin", "<i4"), ("key_end", "<i4")])
+ITEM_DTYPE = np.dtype([("range_begin", "<i4"), ("num_ranges", "<i4"), ("range_keys", "<i4"), ("user_begin", "<i4"),
+                       ("num_users", "<i4"), ("reserved", "<i4")])
 USER_DTYPE = np.dtype([("request", "<i4"), ("pos_offset", "<i4"), ("slot", "<i4"), ("reserved", "<i4")])
-assert ITEM_DTYPE.itemsize == 40 and USER_DTYPE.itemsize == 16
+assert RANGE_DTYPE.itemsize == 32 and ITEM_DTYPE.itemsize == 24 and USER_DTYPE.itemsize == 16
+SHARED_MAX_RANGES = 64  # LAZY_SHARED_MAX_RANGES
 
 _ATTN_PREFILL = [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_i32, _c_i32,
                  _c_i32, _c_p, _c_p, _c_p, _c_sz, _c_p]
@@ -69,9 +72,10 @@ SIGNATURES = {
     "lazy_attn_validate": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64,
                                     ctypes.POINTER(_c_i64), ctypes.POINTER(ctypes.c_char_p)]),
     "lazy_shared_decode_plan": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_i32, _c_i32, _c_p, _c_i32,
-                                         _c_p, _c_i32, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32), _c_p]),
+                                         _c_p, _c_i32, _c_p, _c_i32, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32),
+                                         ctypes.POINTER(_c_i32), _c_p]),
     "lazy_attn_decode_shared": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_p,
-                                         _c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_sz, _c_p]),
+                                         _c_p, _c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_sz, _c_p]),
     "lazy_attn_decode_shared_workspace_size": (_c_sz, [ctypes.POINTER(LazyAttnParams), _c_i32, _c_i32]),
     "lazy_pool_create": (_c_p, [_c_i32]),
     "lazy_pool_destroy": (None, [_c_p]),
@@ -318,12 +322,23 @@ class SharedPlan:
     """A chunk-major shared-decode plan (host arrays from lazy_shared_decode_plan)."""
 
     items: np.ndarray       # ITEM_DTYPE
+    ranges: np.ndarray      # RANGE_DTYPE
     users: np.ndarray       # USER_DTYPE
     slot_start: np.ndarray  # int32 [batch+1]
 
     @property
     def max_slots(self) -> int:
         return int(np.diff(self.slot_start).max()) if self.slot_start.size > 1 else 0
+
+    def item_keys(self) -> np.ndarray:
+        """Keys of every item's run."""
+        last = self.ranges[self.items["range_begin"] + self.items["num_ranges"] - 1]
+        return ((self.items["num_ranges"].astype(np.int64) - 1) * self.items["range_keys"]
+                + (last["key_end"] - last["key_begin"]))
+
+    def read_keys(self) -> int:
+        """Keys read per KV head by one shared-decode launch: every item reads its run once."""
+        return int(self.item_keys().sum()) if self.items.size else 0
 
 
 def shared_decode_plan(cfg: Config, chunks: np.ndarray, chunk_start, max_keys_per_item: int = 0) -> SharedPlan:
@@ -334,26 +349,30 @@ def shared_decode_plan(cfg: Config, chunks: np.ndarray, chunk_start, max_keys_pe
     step = max_keys_per_item or 1024
     cap = max(1, int(np.sum((chunks["len"].astype(np.int64) + step - 1) // step)) if chunks.size else 1)
     p = cfg.c()
-    n_items, n_users = _c_i32(0), _c_i32(0)
+    n_items, n_ranges, n_users = _c_i32(0), _c_i32(0), _c_i32(0)
     slot_start = np.zeros(batch + 1, dtype=np.int32)
     for _ in range(2):
         items = np.zeros(cap, dtype=ITEM_DTYPE)
+        ranges = np.zeros(cap, dtype=RANGE_DTYPE)
         users = np.zeros(cap, dtype=USER_DTYPE)
         code = lib().lazy_shared_decode_plan(ctypes.byref(p), chunks.ctypes.data if chunks.size else None,
                                              cs.ctypes.data, batch, max_keys_per_item, items.ctypes.data, cap,
-                                             users.ctypes.data, cap, ctypes.byref(n_items), ctypes.byref(n_users),
-                                             slot_start.ctypes.data)
-        if code == LAZY_EINVAL and max(n_items.value, n_users.value) > cap:
-            cap = max(n_items.value, n_users.value)
+                                             ranges.ctypes.data, cap, users.ctypes.data, cap, ctypes.byref(n_items),
+                                             ctypes.byref(n_ranges), ctypes.byref(n_users), slot_start.ctypes.data)
+        need = max(n_items.value, n_ranges.value, n_users.value)
+        if code == LAZY_EINVAL and need > cap:
+            cap = need
             continue
         _check(code, "lazy_shared_decode_plan")
-        return SharedPlan(items[: n_items.value].copy(), users[: n_users.value].copy(), slot_start)
+        return SharedPlan(items[: n_items.value].copy(), ranges[: n_ranges.value].copy(), users[: n_users.value].copy(),
+                          slot_start)
     raise RuntimeError("lazy_shared_decode_plan: capacity did not converge")
 
 
 @dataclass
 class DevicePlan:
     items: torch.Tensor
+    ranges: torch.Tensor
     users: torch.Tensor
     slot_start: torch.Tensor
     num_items: int
@@ -364,8 +383,8 @@ def upload_plan(plan: SharedPlan, device="cuda") -> DevicePlan:
     def raw(a):
         b = np.ascontiguousarray(a).view(np.uint8).reshape(-1)
         return torch.from_numpy(b.copy() if b.size else np.zeros(16, np.uint8)).to(device)
-    return DevicePlan(raw(plan.items), raw(plan.users), torch.from_numpy(plan.slot_start.copy()).to(device),
-                      int(plan.items.size), plan.max_slots)
+    return DevicePlan(raw(plan.items), raw(plan.ranges), raw(plan.users),
+                      torch.from_numpy(plan.slot_start.copy()).to(device), int(plan.items.size), plan.max_slots)
 
 
 def decode_shared_workspace_size(cfg: Config, batch: int, max_slots: int) -> int:
@@ -395,7 +414,8 @@ def decode_shared(cfg: Config, q, q_pos, k_pool, v_pool, plan: DevicePlan, out=N
     p = cfg.c()
     _check(lib().lazy_attn_decode_shared(ctypes.byref(p), q.data_ptr(), q_pos.data_ptr(), k_pool.data_ptr(),
                                          v_pool.data_ptr(), plan.items.data_ptr(), plan.num_items,
-                                         plan.users.data_ptr(), plan.slot_start.data_ptr(), batch, plan.max_slots,
+                                         plan.ranges.data_ptr(), plan.users.data_ptr(), plan.slot_start.data_ptr(),
+                                         batch, plan.max_slots,
                                          out.data_ptr(), _ptr(lse), _ptr(workspace), nbytes, _stream(stream)),
            "lazy_attn_decode_shared")
     return out, lse

@@ -260,56 +260,72 @@ def test_shared_plan_layout_matches_header(tmp_path, ops):
     src.write_text(
         '#include <stdio.h>\n#include <stddef.h>\n#include "lazy_attn.h"\n'
         "int main(void){"
-        'printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(lazy_shared_item_t),'
-        " offsetof(lazy_shared_item_t, v_offset), offsetof(lazy_shared_item_t, k_stride),"
-        " offsetof(lazy_shared_item_t, v_stride), offsetof(lazy_shared_item_t, key_begin),"
-        " offsetof(lazy_shared_item_t, key_end), offsetof(lazy_shared_item_t, user_begin),"
-        " offsetof(lazy_shared_item_t, num_users), sizeof(lazy_shared_user_t));"
-        'printf("%zu %zu %zu\\n", offsetof(lazy_shared_user_t, pos_offset), offsetof(lazy_shared_user_t, slot),'
-        " offsetof(lazy_shared_user_t, reserved));"
+        'printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(lazy_shared_range_t), offsetof(lazy_shared_range_t, v_offset),'
+        " offsetof(lazy_shared_range_t, k_stride), offsetof(lazy_shared_range_t, v_stride),"
+        " offsetof(lazy_shared_range_t, key_begin), offsetof(lazy_shared_range_t, key_end));"
+        'printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(lazy_shared_item_t), offsetof(lazy_shared_item_t, num_ranges),'
+        " offsetof(lazy_shared_item_t, range_keys), offsetof(lazy_shared_item_t, user_begin),"
+        " offsetof(lazy_shared_item_t, num_users), offsetof(lazy_shared_item_t, reserved));"
+        'printf("%zu %zu %zu %zu %d\\n", sizeof(lazy_shared_user_t), offsetof(lazy_shared_user_t, pos_offset),'
+        " offsetof(lazy_shared_user_t, slot), offsetof(lazy_shared_user_t, reserved), LAZY_SHARED_MAX_RANGES);"
         "return 0;}"
     )
     exe = tmp_path / "plan_layout"
     subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
-    a, b = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")[:2]
-    it = ops.ITEM_DTYPE
-    us = ops.USER_DTYPE
-    assert [int(x) for x in a.split()] == [it.itemsize] + [it.fields[n][1] for n in (
-        "v_offset", "k_stride", "v_stride", "key_begin", "key_end", "user_begin", "num_users")] + [us.itemsize]
-    assert [int(x) for x in b.split()] == [us.fields[n][1] for n in ("pos_offset", "slot", "reserved")]
+    a, b, c = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")[:3]
+    rg, it, us = ops.RANGE_DTYPE, ops.ITEM_DTYPE, ops.USER_DTYPE
+    assert [int(x) for x in a.split()] == [rg.itemsize] + [rg.fields[n][1] for n in (
+        "v_offset", "k_stride", "v_stride", "key_begin", "key_end")]
+    assert [int(x) for x in b.split()] == [it.itemsize] + [it.fields[n][1] for n in (
+        "num_ranges", "range_keys", "user_begin", "num_users", "reserved")]
+    assert [int(x) for x in c.split()] == [us.itemsize] + [us.fields[n][1] for n in ("pos_offset", "slot", "reserved")] \
+        + [ops.SHARED_MAX_RANGES]
 
 
-def _check_plan(w, plan, g, step):
-    """Invariants of a plan: every piece of every record is exactly one (user, item) pair with the record's stored
-    range, offset and request; slots of a request are 0.. in table order; items respect the column budget and are
-    sorted by key count."""
+def _check_plan(w, plan, g, step, local=False):
+    """Invariants of a plan.  Expanding every (item, user, key of the item's run) gives (request, position, stored
+    key), which must be exactly the keys of the decode tables, each once.  Every (request, slot) belongs to one
+    (item, user) and a request's slots are 0..n-1; items respect the column budget, the range rules (all ranges but
+    the last hold range_keys keys, a multiple of 32 when there are several) and are sorted by run length."""
     per_item = 16 // g
-    seen = {}
-    for it in plan.items:
-        assert 1 <= it["num_users"] <= per_item
-        assert 0 <= it["key_begin"] < it["key_end"] and it["key_end"] - it["key_begin"] <= step
+    got, slots = [], {}
+    keys = plan.item_keys()
+    for n, it in enumerate(plan.items):
+        assert 1 <= it["num_users"] <= per_item and it["reserved"] == 0
+        nr, rk = int(it["num_ranges"]), int(it["range_keys"])
+        assert 1 <= nr <= ops_max_ranges and keys[n] <= step
+        rgs = plan.ranges[it["range_begin"]: it["range_begin"] + nr]
+        lens = rgs["key_end"] - rgs["key_begin"]
+        assert np.all(rgs["key_begin"] >= 0) and np.all(lens >= 1)
+        assert np.all(lens[:-1] == rk) and 1 <= lens[-1] <= rk
+        if nr > 1:
+            assert rk % 32 == 0 and not local
+        run = [(int(r["k_offset"]), int(r["v_offset"]), int(r["k_stride"]), int(r["v_stride"]), int(r["key_begin"]) + j)
+               for r in rgs for j in range(int(r["key_end"] - r["key_begin"]))]
         for u in plan.users[it["user_begin"]: it["user_begin"] + it["num_users"]]:
+            assert u["reserved"] == 0
             key = (int(u["request"]), int(u["slot"]))
-            assert key not in seen
-            seen[key] = (int(it["k_offset"]), int(it["v_offset"]), int(it["k_stride"]), int(it["v_stride"]),
-                         int(it["key_begin"]), int(it["key_end"]), int(u["pos_offset"]))
-    lens = plan.items["key_end"] - plan.items["key_begin"]
-    assert np.all(np.diff(lens) <= 0)
-    expect = {}
+            assert key not in slots
+            slots[key] = n
+            got.extend((int(u["request"]), int(u["pos_offset"]) + j, run[j]) for j in range(len(run)))
+    assert np.all(np.diff(keys) <= 0)
+    expect = []
     for r in range(w.batch):
-        slot = 0
         for rec in w.chunks[w.chunk_start[r]: w.chunk_start[r + 1]]:
-            for kb in range(0, int(rec["len"]), step):
-                expect[(r, slot)] = (int(rec["k_offset"]), int(rec["v_offset"]), int(rec["k_stride"]),
-                                     int(rec["v_stride"]), kb, min(int(rec["len"]), kb + step), int(rec["pos_offset"]))
-                slot += 1
-        assert plan.slot_start[r + 1] - plan.slot_start[r] == slot
-    assert seen == expect
+            expect.extend((r, int(rec["pos_offset"]) + j, (int(rec["k_offset"]), int(rec["v_offset"]),
+                                                           int(rec["k_stride"]), int(rec["v_stride"]), j))
+                          for j in range(int(rec["len"])))
+        n = int(plan.slot_start[r + 1] - plan.slot_start[r])
+        assert sorted(s for (rr, s) in slots if rr == r) == list(range(n))
+    assert len(got) == len(set(got)) and sorted(got) == sorted(expect)
     assert plan.slot_start[0] == 0
 
 
+ops_max_ranges = 64
+
+
 @pytest.mark.parametrize("step", [0, 100, 1000])
-def test_shared_plan_covers_every_record_piece_once(ops, step):
+def test_shared_plan_covers_every_record_key_once(ops, step):
     w = W.rag_decode(seed=5, batch=9, hq=8, hkv=2, n_chunks=5, chunk_len=300, pool_chunks=7, tail_len=9,
                      tail_cap=16)
     plan = ops.shared_decode_plan(ops.config_of(w), w.chunks, w.chunk_start, step)
@@ -326,6 +342,42 @@ def test_shared_plan_g7_and_zipf_reuse(ops):
     _check_plan(w, plan, 7, 128)
 
 
+@pytest.mark.parametrize("bt,step", [(64, 0), (32, 0), (64, 200), (48, 0), (16, 0)])
+def test_shared_plan_chains_paged_blocks(ops, bt, step):
+    """A paged store (blocks of bt tokens, one record per block) is read in runs of blocks: with block sizes that
+    are multiples of 32 the plan reads exactly the keys of the contiguous store's plan in as many items; other block
+    sizes are not chained (one block per item) but still cover every key once.  A local-position store is never
+    chained."""
+    w = W.rag_decode(seed=8, batch=7, hq=8, hkv=2, n_chunks=4, chunk_len=300, pool_chunks=6, tail_len=40,
+                     tail_cap=100)
+    wp = W.paginate(w, bt, seed=3)
+    cfg = ops.config_of(wp)
+    plan = ops.shared_decode_plan(cfg, wp.chunks, wp.chunk_start, step)
+    _check_plan(wp, plan, 4, step or 1024)
+    base = ops.shared_decode_plan(ops.config_of(w), w.chunks, w.chunk_start, step)
+    if bt % 32 == 0:
+        assert plan.items["num_ranges"].max() > 1
+        if step == 0:
+            assert plan.items.size == base.items.size and plan.read_keys() == base.read_keys()
+    else:
+        assert plan.items["num_ranges"].max() == 1
+    local = ops.shared_decode_plan(ops.config_of(wp, key_positions=ops.KEYS_LOCAL), wp.chunks, wp.chunk_start, step)
+    _check_plan(wp, local, 4, step or 1024, local=True)
+
+
+def test_shared_plan_breaks_runs_where_requests_diverge(ops):
+    """Two requests read the blocks of chunk A and then of different chunks: the run covers A's blocks only."""
+    rec = lambda ko, pos, n=64: (ko, ko + 100000, n, pos, 64, 64)
+    a = [rec(1000 * k, 64 * k) for k in range(3)]
+    t1 = [rec(50000 + 1000 * k, 192 + 64 * k) for k in range(2)]
+    t2 = [rec(80000 + 1000 * k, 192 + 64 * k) for k in range(2)]
+    chunks = np.array(a + t1 + a + t2, dtype=ops.CHUNK_DTYPE)
+    cs = np.array([0, 5, 10], dtype=np.int32)
+    plan = ops.shared_decode_plan(ops.Config(8, 2, 128, 1e4), chunks, cs)
+    runs = sorted((int(it["num_ranges"]), int(it["num_users"])) for it in plan.items)
+    assert runs == [(2, 1), (2, 1), (3, 2)]
+
+
 def test_shared_plan_errors(ops):
     w = W.rag_decode(seed=7, batch=2, hq=8, hkv=2, n_chunks=2, chunk_len=40, pool_chunks=3, tail_len=2, tail_cap=4)
     L = ops.lib()
@@ -333,30 +385,33 @@ def test_shared_plan_errors(ops):
     ch = np.ascontiguousarray(w.chunks)
     cs = np.ascontiguousarray(w.chunk_start, dtype=np.int32)
     items = np.zeros(1, dtype=ops.ITEM_DTYPE)
+    ranges = np.zeros(1, dtype=ops.RANGE_DTYPE)
     users = np.zeros(1, dtype=ops.USER_DTYPE)
-    ni, nu = ctypes.c_int32(0), ctypes.c_int32(0)
+    ni, nr, nu = ctypes.c_int32(0), ctypes.c_int32(0), ctypes.c_int32(0)
     ss = np.zeros(3, dtype=np.int32)
     code = L.lazy_shared_decode_plan(ctypes.byref(p), ch.ctypes.data, cs.ctypes.data, 2, 0, items.ctypes.data, 1,
-                                     users.ctypes.data, 1, ctypes.byref(ni), ctypes.byref(nu), ss.ctypes.data)
-    assert code == ops.LAZY_EINVAL and ni.value > 1 and nu.value == len(w.chunks)  # capacity: counts still reported
+                                     ranges.ctypes.data, 1, users.ctypes.data, 1, ctypes.byref(ni), ctypes.byref(nr),
+                                     ctypes.byref(nu), ss.ctypes.data)
+    assert code == ops.LAZY_EINVAL and ni.value > 1 and nr.value > 1 and nu.value == len(w.chunks)  # counts reported
     big = ops.Config(34, 2, 128, 1e4)  # G = 17 columns do not fit one workgroup
     pb = big.c()
-    assert L.lazy_shared_decode_plan(ctypes.byref(pb), ch.ctypes.data, cs.ctypes.data, 2, 0, None, 0, None, 0,
-                                     ctypes.byref(ni), ctypes.byref(nu), ss.ctypes.data) == ops.LAZY_EUNSUPPORTED
+    args = lambda pp, c, step: (ctypes.byref(pp), c.ctypes.data, cs.ctypes.data, 2, step, None, 0, None, 0, None, 0,
+                                ctypes.byref(ni), ctypes.byref(nr), ctypes.byref(nu), ss.ctypes.data)
+    assert L.lazy_shared_decode_plan(*args(pb, ch, 0)) == ops.LAZY_EUNSUPPORTED
     bad = ch.copy()
     bad["len"][1] = -3
-    assert L.lazy_shared_decode_plan(ctypes.byref(p), bad.ctypes.data, cs.ctypes.data, 2, 0, None, 0, None, 0,
-                                     ctypes.byref(ni), ctypes.byref(nu), ss.ctypes.data) == ops.LAZY_EDATA
-    assert L.lazy_shared_decode_plan(ctypes.byref(p), ch.ctypes.data, cs.ctypes.data, 2, -1, None, 0, None, 0,
-                                     ctypes.byref(ni), ctypes.byref(nu), ss.ctypes.data) == ops.LAZY_EINVAL
+    assert L.lazy_shared_decode_plan(*args(p, bad, 0)) == ops.LAZY_EDATA
+    assert L.lazy_shared_decode_plan(*args(p, ch, -1)) == ops.LAZY_EINVAL
     # scalar checks of the device entry point (no launch)
-    assert L.lazy_attn_decode_shared(ctypes.byref(pb), 1, 1, 1, 1, 1, 1, 1, 1, 2, 1, 1, None, None, 0,
+    assert L.lazy_attn_decode_shared(ctypes.byref(pb), 1, 1, 1, 1, 1, 1, 1, 1, 1, 2, 1, 1, None, None, 0,
                                      None) == ops.LAZY_EUNSUPPORTED
-    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, 1, 1, 2, 0, 1, None, None, 0,
+    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, 1, 1, 1, 2, 0, 1, None, None, 0,
                                      None) == ops.LAZY_EINVAL
-    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, 1, 1, 2, 4, 1, None, None, 0,
+    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, None, 1, 1, 2, 4, 1, None, None, 0,
+                                     None) == ops.LAZY_EINVAL                                # ranges missing
+    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, 1, 1, 1, 2, 4, 1, None, None, 0,
                                      None) == ops.LAZY_EWORKSPACE
-    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, 1, 1, 0, 4, 1, None, None, 0,
+    assert L.lazy_attn_decode_shared(ctypes.byref(p), 1, 1, 1, 1, 1, 3, 1, 1, 1, 0, 4, 1, None, None, 0,
                                      None) == ops.LAZY_OK
     assert ops.decode_shared_workspace_size(ops.config_of(w), 2, 5) == 5 * 2 * 8 * (2 * 128 + 4)
 
@@ -364,37 +419,56 @@ def test_shared_plan_errors(ops):
 @pytest.mark.skipif(shutil.which("g++") is None, reason="g++ missing")
 def test_shared_plan_under_address_and_ub_sanitizers(tmp_path):
     drv = tmp_path / "plan_drv.cpp"
-    drv.write_text(r'''
+    drv.write_text(r"""
 #include <stdio.h>
 #include <vector>
 #include "lazy_attn.h"
 int main() {
   lazy_attn_params_t p = {8, 2, 128, 1, 1e4f, 0.f, nullptr, 0, 0};
-  // 3 requests; records 0/2/4 read the same stored chunk at different offsets, one 2500-key private record
+  // 3 requests; records 0/2/4 read the same stored chunk at different offsets, one 2500-key private record, and a
+  // paged run (64-key blocks 5..7 then 8..9) that requests 1 and 2 both read
   std::vector<lazy_chunk_t> c = {{0, 4096, 300, 0, 300, 300}, {9000, 9500, 20, 300, 32, 32},
                                  {0, 4096, 300, 50, 300, 300}, {20000, 90000, 2500, 0, 2500, 2500},
-                                 {0, 4096, 300, 7, 300, 300}};
+                                 {0, 4096, 300, 7, 300, 300},
+                                 {100000, 200000, 64, 3000, 64, 64}, {101000, 201000, 64, 3064, 64, 64},
+                                 {102000, 202000, 10, 3128, 64, 64},
+                                 {100000, 200000, 64, 4000, 64, 64}, {101000, 201000, 64, 4064, 64, 64},
+                                 {102000, 202000, 10, 4128, 64, 64}};
   int32_t cs[4] = {0, 2, 4, 5};
+  int32_t cs2[4] = {0, 2, 8, 11};
   int fails = 0;
-  for (int step : {0, 1, 64, 1000}) {
-    int32_t ni = 0, nu = 0, ss[4];
-    int code = lazy_shared_decode_plan(&p, c.data(), cs, 3, step, nullptr, 0, nullptr, 0, &ni, &nu, ss);
-    if (code != LAZY_EINVAL || ni <= 0 || nu <= 0) ++fails;
-    std::vector<lazy_shared_item_t> items(ni);
-    std::vector<lazy_shared_user_t> users(nu);
-    code = lazy_shared_decode_plan(&p, c.data(), cs, 3, step, items.data(), ni, users.data(), nu, &ni, &nu, ss);
-    if (code != LAZY_OK || ss[0] != 0 || ss[3] != nu) ++fails;
-    for (const auto& it : items)
-      if (it.user_begin < 0 || it.user_begin + it.num_users > nu || it.num_users < 1 || it.num_users > 4) ++fails;
-  }
-  int32_t ni = 0, nu = 0, ss[4];
-  if (lazy_shared_decode_plan(&p, nullptr, cs, 3, 0, nullptr, 0, nullptr, 0, &ni, &nu, ss) != LAZY_EINVAL) ++fails;
+  for (int local = 0; local < 2; ++local)
+    for (const int32_t* table : {cs, cs2})
+      for (int step : {0, 1, 64, 200, 1000}) {
+        p.key_positions = local;
+        int32_t ni = 0, nr = 0, nu = 0, ss[4];
+        int code = lazy_shared_decode_plan(&p, c.data(), table, 3, step, nullptr, 0, nullptr, 0, nullptr, 0, &ni,
+                                           &nr, &nu, ss);
+        if (code != LAZY_EINVAL || ni <= 0 || nr <= 0 || nu <= 0) ++fails;
+        std::vector<lazy_shared_item_t> items(ni);
+        std::vector<lazy_shared_range_t> ranges(nr);
+        std::vector<lazy_shared_user_t> users(nu);
+        code = lazy_shared_decode_plan(&p, c.data(), table, 3, step, items.data(), ni, ranges.data(), nr,
+                                       users.data(), nu, &ni, &nr, &nu, ss);
+        if (code != LAZY_OK || ss[0] != 0 || ss[3] > nu) ++fails;
+        for (const auto& it : items) {
+          if (it.user_begin < 0 || it.user_begin + it.num_users > nu || it.num_users < 1 || it.num_users > 4) ++fails;
+          if (it.range_begin < 0 || it.num_ranges < 1 || it.range_begin + it.num_ranges > nr) ++fails;
+          if (local && it.num_ranges != 1) ++fails;
+        }
+      }
+  int32_t ni = 0, nr = 0, nu = 0, ss[4];
+  if (lazy_shared_decode_plan(&p, nullptr, cs, 3, 0, nullptr, 0, nullptr, 0, nullptr, 0, &ni, &nr, &nu, ss) !=
+      LAZY_EINVAL)
+    ++fails;
   int32_t empty[1] = {0};
-  if (lazy_shared_decode_plan(&p, nullptr, empty, 0, 0, nullptr, 0, nullptr, 0, &ni, &nu, ss) != LAZY_OK) ++fails;
+  if (lazy_shared_decode_plan(&p, nullptr, empty, 0, 0, nullptr, 0, nullptr, 0, nullptr, 0, &ni, &nr, &nu, ss) !=
+      LAZY_OK)
+    ++fails;
   printf("sanitized planner ok=%d\n", fails == 0);
   return fails;
 }
-''')
+""")
     exe = tmp_path / "plan_drv"
     subprocess.run(["g++", "-std=c++17", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-I",
                     os.path.join(ROOT, "include"), str(drv), os.path.join(B.CSRC, "lazy_attn_plan.cpp"), "-o",

@@ -487,6 +487,24 @@ def test_paged_decode_matches_oracle_per_request_and_shared(bt):
         run_shared_and_check(w, f"paged{bt} shared decode {'local' if local else 'nope'}", ckw)
 
 
+@pytest.mark.parametrize("mode", ["nope", "interleaved", "alibi", "prerotated"])
+@pytest.mark.parametrize("bt,step", [(64, 0), (32, 100), (64, 160), (128, 0)])
+def test_shared_decode_multi_range_runs(bt, step, mode):
+    """Paged stores read in runs of blocks (items of several ranges): tiles cross range boundaries at multiples of
+    32 keys, runs are capped by the item size, and the last range of a run is partial.  G = 4 and G = 7 (d = 64)."""
+    for kw in (dict(seed=121, batch=6, hq=8, hkv=2, d=128, n_chunks=4, chunk_len=250, pool_chunks=5, tail_len=41,
+                    tail_cap=64),
+               dict(seed=122, batch=4, hq=14, hkv=2, d=64, n_chunks=3, chunk_len=333, pool_chunks=4, tail_len=3,
+                    tail_cap=40)):
+        w = W.paginate(W.rag_decode(**kw), bt, seed=bt + step)
+        cfg = {"nope": {}, "interleaved": IL, "alibi": ALIBI, "prerotated": {}}[mode]
+        if mode == "prerotated":
+            check_prerotated(w, f"runs bt{bt} step{step} prerotated", {}, shared=True)
+            continue
+        plan = run_shared_and_check(w, f"runs bt{bt} step{step} {mode} d{kw['d']}", cfg, step)
+        assert plan.items["num_ranges"].max() > 1
+
+
 # --------------------------------------------------------------------------------------------------------------
 # Interleaved RoPE pairing (pairs (2t, 2t+1), Sec. 3.5): every kernel, both key conventions.
 IL = dict(rope_style=ops.ROPE_INTERLEAVED)
