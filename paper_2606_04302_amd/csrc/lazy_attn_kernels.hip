@@ -894,13 +894,18 @@ struct DecodeSmem {
   static constexpr int CSD_LD = D + 4;               // per-row cos/sin row stride (floats): 4 banks per row
   static constexpr int CSB = D + D / 4;              // per-tile base table: (c, s) of pair t at 2t + 4*(t/8)
   uint16_t v[4][kDecWaveKeys * VLD] __attribute__((aligned(16)));
-  float csd[kDecWaveKeys * CSD_LD] __attribute__((aligned(16)));
+  float csd[kDecWaveKeys * CSD_LD + 32] __attribute__((aligned(16)));  // row r at dec_row(r)
   float csb[4][2][CSB] __attribute__((aligned(16)));
   u32x4 qsave[D / 64][2][64];                       // raw Q fragments [s][half][lane] (local-position keys)
   double freq[D / 2];
 };
 template <int D>
 __device__ __forceinline__ int csb_idx(int t) { return 2 * t + 4 * (t >> 3); }
+// Start of row r of the per-row cos/sin table.  The 16 lanes of one 16-byte read pass take rows kappa(b, 0..15) =
+// {0..7, 16..23} + 8b at one column; rows 16 apart would share banks (16 x 4-bank shift = 64 banks), so rows
+// 16..31 are moved 32 banks further.
+template <int D>
+__device__ __forceinline__ int dec_row(int r) { return r * DecodeSmem<D>::CSD_LD + 32 * (r >> 4); }
 
 // Raw K / V of one wave tile in registers.
 template <int D>
@@ -1129,7 +1134,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // Per-row constants cos/sin(delta theta_t), delta < 32: 16 per thread.
     for (int e = tid; e < kDecWaveKeys * (D / 2); e += kThreads) {
       const int dr = e / (D / 2), t = e % (D / 2);
-      *reinterpret_cast<float2*>(sm.csd + dr * S::CSD_LD + 2 * t) = rope_cs(dr, sm.freq[t]);
+      *reinterpret_cast<float2*>(sm.csd + dec_row<D>(dr) + 2 * t) = rope_cs(dr, sm.freq[t]);
     }
     if (have && lane < D / 2)
       *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
@@ -1185,8 +1190,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // Transposing-read address of this lane in its V slice: row 16*(kq/2) + 4*(kq%2) + i/4 (+ 8 for the second
   // half), column 4*(i%4) (+ 16 per dimension block); i = lane % 16.
   const uint16_t* vlane = vw + (16 * (kq >> 1) + 4 * (kq & 1) + ((lane & 15) >> 2)) * S::VLD + 4 * (lane & 3);
-  const float* cd0 = sm.csd + kappa(0, col) * S::CSD_LD;
-  const float* cd1 = sm.csd + kappa(1, col) * S::CSD_LD;
+  const float* cd0 = sm.csd + dec_row<D>(kappa(0, col));
+  const float* cd1 = sm.csd + dec_row<D>(kappa(1, col));
   int buf = 0;
   while (have) {
     const int nvalid = min(kDecWaveKeys, it.cur.len - it.j0);
@@ -1356,7 +1361,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   if (ROT) {
     for (int e = tid; e < kDecWaveKeys * (D / 2); e += kThreads) {
       const int dr = e / (D / 2), t = e % (D / 2);
-      *reinterpret_cast<float2*>(sm.csd + dr * S::CSD_LD + 2 * t) = rope_cs(dr, sm.freq[t]);
+      *reinterpret_cast<float2*>(sm.csd + dec_row<D>(dr) + 2 * t) = rope_cs(dr, sm.freq[t]);
     }
     if (tile < ntiles && lane < D / 2)
       *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(kDecWaveKeys * tile, sm.freq[lane]);
@@ -1404,8 +1409,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const float ab = ALIBI ? alibi_slope(g * G + col % G, a.hq, a.inv_freq, c) : 0.f;
   uint16_t* vw = sm.v[wave];
   const uint16_t* vlane = vw + (16 * (kq >> 1) + 4 * (kq & 1) + ((lane & 15) >> 2)) * S::VLD + 4 * (lane & 3);
-  const float* cd0 = sm.csd + kappa(0, col) * S::CSD_LD;
-  const float* cd1 = sm.csd + kappa(1, col) * S::CSD_LD;
+  const float* cd0 = sm.csd + dec_row<D>(kappa(0, col));
+  const float* cd1 = sm.csd + dec_row<D>(kappa(1, col));
   int buf = 0;
   while (tile < ntiles) {
     const int j0 = kDecWaveKeys * tile;
