@@ -97,6 +97,20 @@ def timed_graph(fn, reps: int, inner: int = 20):
     return start.elapsed_time(end) / (reps * inner)
 
 
+def timed_median(fn, loops: int = 20, inner: int = 10):
+    """Median over ``loops`` timed loops of ``inner`` back-to-back calls (ms per call), after the caller's warm-up."""
+    import torch
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(loops)]
+    for a, b in ev:
+        a.record()
+        for _ in range(inner):
+            fn()
+        b.record()
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) / inner for a, b in ev]))
+
+
 def timed_cold(fn, reps: int, scrub_mib: int = 512):
     """Average ms per call with cold caches: before every call a 512 MiB buffer (twice the 256 MB MALL, far more than
     the L2s) is overwritten, then the call alone is bracketed by HIP events.  The scrub is queued ahead of the call,
@@ -136,12 +150,22 @@ def cpu_baseline(w, flops_per_pass: float, budget_s: float = 12.0):
         if el >= budget_s or passes >= 50:
             break
     per = el / passes
+    model = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover - informational only
+        pass
     return {
         "value": flops_per_pass / per / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"full rag_prefill batch (8 requests), {passes} pass(es), {per:.2f} s per pass, numpy fp64",
+        "sample": f"full rag_prefill batch (8 requests), {passes} pass(es), {per:.2f} s per pass, numpy fp64 with "
+                  f"{int(threads)} BLAS threads on {model} ({os.cpu_count()} logical CPUs visible)",
         "s_per_pass": per,
     }
 
@@ -451,6 +475,8 @@ def main() -> int:
         combine_ms = timed_graph(lambda: ops.combine(part_o, part_lse, out=out2, lse=lse2), max(20, args.steps // 4))
     kernel_ms = ms - combine_ms
 
+    median_ms = timed_median(prefill)
+
     # Cold caches: every launch after a 512 MiB scrub, so the store comes from HBM and not from the MALL / L2s.
     cold_ms = timed_cold(prefill, max(10, args.steps // 10))
 
@@ -534,6 +560,7 @@ def main() -> int:
             "kernel_ms": round(kernel_ms, 5),
             "combine_ms": round(combine_ms, 5),
             "logical_hbm_gbps": round(alg_bytes / (ms * 1e-3) / 1e9, 1),
+            "median_of_20_loops_ms": round(median_ms, 5),
             "cold_cache_ms": round(cold_ms, 5),
             "cold_cache_tflops": round(flops / (cold_ms * 1e-3) / 1e12, 3),
             "no_rotation_ms": round(norot_ms, 5),
