@@ -1301,7 +1301,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 // K / V address of key j (within the run) of KV head g: range j / rk of the run, whose ranges are staged in LDS.
 __device__ __forceinline__ void run_key(const lazy_shared_range_t* rg, int nr, int rk, int g, int j, int d,
                                         int64_t& koff, int64_t& voff) {
-  const int r = nr == 1 ? 0 : j / rk;
+  const int r = nr == 1 ? 0 : min(j / rk, nr - 1);
   const int jr = j - r * rk + rg[r].key_begin;
   koff = rg[r].k_offset + ((int64_t)g * rg[r].k_stride + jr) * d;
   voff = rg[r].v_offset + ((int64_t)g * rg[r].v_stride + jr) * d;
@@ -1321,7 +1321,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   __shared__ lazy_shared_range_t srg[LAZY_SHARED_MAX_RANGES];
   const cptr<lazy_shared_item_t> item = as_const(a.items) + blockIdx.x;
   const int g = blockIdx.y;
-  const int rb = item->range_begin, nr = item->num_ranges, rk = item->range_keys;
+  // Item fields come from the planner; the clamps keep the LDS range table in bounds for any values.
+  const int rb = item->range_begin, nr = max(1, min(item->num_ranges, LAZY_SHARED_MAX_RANGES));
+  const int rk = max(1, item->range_keys);
   const int u0 = item->user_begin, nu = item->num_users;
   const cptr<lazy_shared_range_t> rgs = as_const(a.ranges) + rb;
   const int nk = (nr - 1) * rk + (rgs[nr - 1].key_end - rgs[nr - 1].key_begin);  // keys of the run
@@ -1349,7 +1351,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   DecTile<D> cur, nxt;
   if (tile < ntiles) {  // the first tile straight from the range table (the LDS copy is not ready yet)
     const int j0 = kDecWaveKeys * tile;
-    const int r = nr == 1 ? 0 : j0 / rk;
+    const int r = nr == 1 ? 0 : min(j0 / rk, nr - 1);
     const int jr = j0 - r * rk + rgs[r].key_begin;
     dec_fetch<D, IL>(cur, a.k_pool + rgs[r].k_offset + ((int64_t)g * rgs[r].k_stride + jr) * D,
                      a.v_pool + rgs[r].v_offset + ((int64_t)g * rgs[r].v_stride + jr) * D,
