@@ -452,17 +452,23 @@ def test_shared_decode_edge_cases():
     run_shared_and_check(w, "shared edge non-causal")
 
 
-def test_shared_decode_full_size_sampled():
-    """The benchmark's decode batch (64 requests, chunks shared ~4x) through the shared path, sampled requests."""
+@pytest.mark.parametrize("paged", [False, True])
+def test_shared_decode_full_size_sampled(paged):
+    """The benchmark's decode batch (64 requests, chunks shared ~4x) through the shared path, sampled requests; also
+    over the benchmark's paged store (64-token blocks), read in block runs."""
     w = W.rag_decode(seed=2)
+    if paged:
+        w = W.paginate(w, 64, seed=7)
     cfg = ops.config_of(w)
     plan = ops.shared_decode_plan(cfg, w.chunks, w.chunk_start)
+    if paged:
+        assert plan.items["num_ranges"].max() == 16 and plan.items.size == 424
     dw = ops.upload(w)
     out, _ = ops.decode_shared(cfg, dw.q, dw.q_pos0, dw.pool, dw.pool, ops.upload_plan(plan))
     torch.cuda.synchronize()
     ref_o, ref_l = oracle(w, requests=[0, 31, 63])
     rows = rows_of(w, [0, 31, 63])
-    assert_close(out, None, ref_o, ref_l, rows, tag="shared full rag_decode")
+    assert_close(out, None, ref_o, ref_l, rows, tag=f"shared full rag_decode {'paged64' if paged else ''}")
 
 
 # --------------------------------------------------------------------------------------------------------------
