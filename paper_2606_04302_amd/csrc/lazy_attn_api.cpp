@@ -46,6 +46,11 @@ int prefill_q_tiles(const lazy_attn_params_t* p, int32_t max_q_len) {
   return (int)ceil_div((int64_t)max_q_len * g, (int64_t)lazy::kPrefillRowsPerBlock * prefill_row_blocks(p, max_q_len));
 }
 
+// A batch is ragged when its mean query length is below 3/4 of the maximum.
+bool prefill_ragged(int32_t batch, int32_t total_q, int32_t max_q_len) {
+  return 4 * (int64_t)total_q < 3 * (int64_t)batch * max_q_len;
+}
+
 // KV splits per request.  Workgroups are (query tile, KV head, request, split); those of a query tile past the end
 // of a shorter request exit at once, so the busy ones number about Hkv * ceil(total_q G / rows per tile) per split.
 // Equal requests: one round of workgroups over the chip.  Ragged query lengths (mean below 3/4 of the maximum)
@@ -60,8 +65,7 @@ int prefill_splits(const lazy_attn_params_t* p, int32_t batch, int32_t total_q, 
   const int64_t tiles = ceil_div(max_kv_len, lazy::kPrefillTileKeys);
   // 256-row workgroups occupy a whole CU (LDS), 128-row ones leave room for two per CU.
   const int64_t slots = prefill_row_blocks(p, max_q_len) == 2 ? kNumCUs : 2 * kNumCUs;
-  const bool ragged = 4 * (int64_t)total_q < 3 * (int64_t)batch * max_q_len;
-  const int64_t target = ragged ? 3 * slots : slots;
+  const int64_t target = prefill_ragged(batch, total_q, max_q_len) ? 3 * slots : slots;
   int64_t s = busy > 0 ? ceil_div(target, busy) : 1;
   const int64_t cap = tiles / 4 > 1 ? tiles / 4 : 1;  // keep at least ~4 key tiles per split
   if (s > cap) s = cap;
@@ -136,6 +140,8 @@ int run_prefill(bool rotate_k, const lazy_attn_params_t* p, const void* q, const
   a.splits = splits;
   a.q_tiles = q_tiles;
   a.row_blocks = prefill_row_blocks(p, max_q_len);
+  // Ragged batches spread their (request, split) units over the XCDs; alike requests keep whole requests per XCD.
+  a.xcd_interleave = prefill_ragged(batch, total_q, max_q_len);
   a.head_groups = 1;
   a.rope_log2_base = p->inv_freq || p->rope_style == LAZY_ALIBI ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);

@@ -31,6 +31,7 @@ struct AttnArgs {
   int32_t splits;
   int32_t q_tiles;            // prefill: row tiles per (request, kv head)
   int32_t row_blocks;         // prefill: a workgroup covers 128 * row_blocks packed rows (2 = eight-wave kernel)
+  int32_t xcd_interleave;     // prefill: 1 spreads (request, split) units over the XCDs (ragged batches)
   int32_t head_groups;        // decode: ceil(group / 16)
   int32_t local_keys;         // 1: the store holds keys encoded at local positions (LAZY_KEYS_LOCAL)
   int32_t interleaved;        // 1: RoPE pairs (2t, 2t+1) (LAZY_ROPE_INTERLEAVED)

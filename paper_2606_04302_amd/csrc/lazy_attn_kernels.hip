@@ -385,9 +385,20 @@ __device__ __forceinline__ const uint16_t* v_ptr(const uint16_t* pool, const Rec
 // double-buffers the LDS tiles (one barrier per tile, the next tile's global loads in flight during the current
 // tile's MFMAs); NBUF = 1 keeps the LDS small enough for two workgroups per CU.
 // ---------------------------------------------------------------------------------------------------------------
-// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).  Remapping the linear workgroup id
-// so that consecutive logical ids share an XCD puts the row tiles that read the same keys onto one L2.
-__device__ __forceinline__ int xcd_remap(int id, int n) {
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2): linear id L runs on XCD L % 8.  Two
+// maps from L to the logical workgroup:
+//  - contiguous (uniform batches): XCD k takes the k-th eighth of the logical ids, i.e. whole requests with all of
+//    their heads and splits, which measured fastest when requests are alike;
+//  - interleaved (ragged batches): the nx row tiles and ny heads of one (request, split) unit z stay on one XCD,
+//    and unit z runs on XCD z % 8 (its XCD's m-th workgroup is tile m % (nx ny) of unit z = L % 8 + 8 (m / (nx ny))),
+//    so requests of different lengths are spread evenly over the XCDs instead of piling onto some of them.
+// Both fall back to the identity where the counts do not divide by 8.
+__device__ __forceinline__ int xcd_remap(int id, int n, int inner, int units, bool interleave) {
+  if (interleave) {
+    if (units & 7) return id;
+    const int m = id >> 3;
+    return m % inner + inner * ((id & 7) + 8 * (m / inner));
+  }
   const int per = n >> 3;
   return id < (per << 3) ? (id & 7) * per + (id >> 3) : id;
 }
@@ -696,7 +707,8 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   constexpr int BM = 32 * NW * RB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nx = gridDim.x, ny = gridDim.y;
-  const int lid = xcd_remap(blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z), nx * ny * gridDim.z);
+  const int lid = uniform(xcd_remap(blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z), nx * ny * gridDim.z, nx * ny,
+                                    gridDim.z, a.xcd_interleave != 0));
   const int qtile = lid % nx;
   const int g = (lid / nx) % ny;
   const int zz = lid / (nx * ny);
