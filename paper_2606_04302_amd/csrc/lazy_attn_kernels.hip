@@ -73,14 +73,17 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // and their waits drain the vector-memory queue that holds the next tile's prefetched K / V.
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
-// Inclusive prefix sum over the 64 lanes of a wave.
+// Inclusive prefix sum over the 64 lanes of a wave (all lanes active), with DPP lane moves instead of LDS
+// permutes: shifts by 1, 2, 4, 8 within each 16-lane row (lanes shifted in from outside the row read 0), then the
+// last lane of row 0 is added to row 1 and that of row 2 to row 3 (row_bcast:15), then the last lane of row 1
+// (the total of rows 0-1) to rows 2 and 3 (row_bcast:31).  Rows left out by the row mask keep their value.
 __device__ __forceinline__ int wave_incl_scan(int x) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15, rows 1 and 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31, rows 2 and 3
   return x;
 }
 // Reductions over lane pairs (l, l ^ 32) with v_permlane32_swap (one VALU op, no LDS round trip).  Swapping a
@@ -216,28 +219,48 @@ struct TileIter {
   // The tile counts are taken one record per lane, 64 records at a time, with a wave-wide prefix sum, so that a long
   // chunk table costs a few parallel loads rather than a chain of dependent ones.  Must be called by whole waves
   // with wave-uniform arguments; every member ends up wave-uniform.
+  //
+  // The loads of the first 256 records come first and on their own (first_block), so that a caller can issue other
+  // loads while they are in flight: record c0 + lane whole (the record holding the split's first tile and the one
+  // after it then come from a lane instead of one more dependent load), and the lengths of records
+  // c0 + 64 (u + 1) + lane.  Indexes past the table's end read its last record and are ignored afterwards, so no
+  // load sits behind a per-lane branch.
+  struct First {
+    lazy_chunk_t mine;
+    int len[3];
+  };
+  __device__ static First first_block(const lazy_chunk_t* table, int c0, int c1) {
+    First f = {};
+    if (c1 > c0) {
+      const int k = c0 + (threadIdx.x & 63);
+      f.mine = table[min(k, c1 - 1)];
+#pragma unroll
+      for (int u = 0; u < 3; ++u) f.len[u] = table[min(k + 64 * (u + 1), c1 - 1)].len;
+    }
+    return f;
+  }
   __device__ void init(const lazy_chunk_t* table, int c0, int c1, int split, int splits) {
+    init(table, c0, c1, split, splits, first_block(table, c0, c1));
+  }
+  __device__ void init(const lazy_chunk_t* table, int c0, int c1, int split, int splits, const First& first) {
     recs = as_const(table);
     end = c1;
     const int lane = threadIdx.x & 63;
-    // Pass 1: the request's tile count.  Four blocks of 64 records are loaded at once; the first four stay in
-    // registers for pass 2.  The first block is loaded whole (one record per lane), so that the record holding the
-    // split's first tile and the one after it come from a lane instead of one more dependent load.
+    const lazy_chunk_t& mine = first.mine;
+    // Pass 1: the request's tile count, four blocks of 64 records at a time; the first four blocks' counts stay in
+    // registers for pass 2.
     int ntiles = 0, ntb[4];
-    lazy_chunk_t mine = {};
-    if (c0 + lane < c1) mine = table[c0 + lane];
     for (int k0 = c0; k0 < c1; k0 += 256) {
-      int nt[4];
+      int nt[4], sum = 0;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int k = k0 + 64 * u + lane;
-        nt[u] = k < c1 ? ((k0 == c0 && u == 0 ? mine.len : table[k].len) + TK - 1) / TK : 0;
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
+        const int len = k0 != c0 ? (k < c1 ? table[k].len : 0) : u == 0 ? mine.len : first.len[u - 1];
+        nt[u] = k < c1 ? (len + TK - 1) / TK : 0;
         if (k0 == c0) ntb[u] = nt[u];
-        ntiles += __builtin_amdgcn_readlane(wave_incl_scan(nt[u]), 63);
+        sum += nt[u];
       }
+      ntiles += __builtin_amdgcn_readlane(wave_incl_scan(sum), 63);
     }
     const int lo = (int)((int64_t)ntiles * split / splits);
     const int hi = (int)((int64_t)ntiles * (split + 1) / splits);
@@ -351,7 +374,8 @@ __device__ __forceinline__ int cs_idx(int t) { return 2 * t + 4 * (t / 32); }
 template <int D>
 __device__ __forceinline__ bf16x8 q_fragment_tab(u32x2 lo, u32x2 hi, int t0, const float* qb, const float* qd,
                                                  bool valid) {
-  if (!valid) return as_bf16x8(u32x4{0, 0, 0, 0});
+  // Rows past the end are computed like the others and zeroed at the end: no per-lane branch, so the waits for the
+  // raw Q loads stay exact (a branch makes the compiler wait for every load in flight, the first tile's included).
   const f32x4 b01 = reinterpret_cast<const f32x4*>(qb + cs_idx<D>(t0))[0];
   const f32x4 b23 = reinterpret_cast<const f32x4*>(qb + cs_idx<D>(t0))[1];
   const f32x4 d01 = reinterpret_cast<const f32x4*>(qd + cs_idx<D>(t0))[0];
@@ -366,7 +390,8 @@ __device__ __forceinline__ bf16x8 q_fragment_tab(u32x2 lo, u32x2 hi, int t0, con
     const int o2 = 2 * (e & 1);
     rotate_pair(x1, x2, make_float2(bq[o2], bq[o2 + 1]), make_float2(dq[o2], dq[o2 + 1]), y1[e], y2[e]);
   }
-  return as_bf16x8(u32x4{pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y2[0], y2[1]), pack2(y2[2], y2[3])});
+  const u32x4 w = {pack2(y1[0], y1[1]), pack2(y1[2], y1[3]), pack2(y2[0], y2[1]), pack2(y2[2], y2[3])};
+  return as_bf16x8(valid ? w : u32x4{0, 0, 0, 0});
 }
 
 __device__ __forceinline__ const uint16_t* k_ptr(const uint16_t* pool, const Rec& r, int g, int j0, int d) {
@@ -734,49 +759,56 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   const int last = min(row0 + BM, nrows) - 1;
   const int qmin = uniform(qp0 + row0 / G), qmax = uniform(qp0 + last / G);
 
-  // Raw Q first, then the chunk-table walk and the first tile's K / V: the angle tables and the Q rotation below
-  // are computed while those loads are in flight (Q, issued first, is waited for without waiting for the tile).
+  // Loads first: the first block of the chunk table and raw Q.  The angle tables below need neither and are computed
+  // while they are in flight.
+  const int c0 = as_const(a.chunk_start)[r], c1 = as_const(a.chunk_start)[r + 1];
+  const TileIter<kSub>::First first = TileIter<kSub>::first_block(a.chunks, c0, c1);
   u32x2 qraw[RB][D / 16][2];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const uint16_t* qrow = a.q + ((int64_t)(qs + tok[rb]) * a.hq + head[rb]) * D;
+    // Rows past the request's end read its first query row (tok 0, head g G: always present, since the request
+    // has a row here) and give zero fragments below; the loads sit behind no per-lane branch.
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
       const int t0 = 8 * s + 4 * h2;
-      qraw[rb][s][0] = qraw[rb][s][1] = u32x2{0, 0};
-      if (rvalid[rb]) {
-        if (IL) {
-          deinterleave4(*reinterpret_cast<const u32x4*>(qrow + 2 * t0), qraw[rb][s][0], qraw[rb][s][1]);
-        } else {
-          qraw[rb][s][0] = *reinterpret_cast<const u32x2*>(qrow + t0);
-          qraw[rb][s][1] = *reinterpret_cast<const u32x2*>(qrow + D / 2 + t0);
-        }
+      if (IL) {
+        deinterleave4(*reinterpret_cast<const u32x4*>(qrow + 2 * t0), qraw[rb][s][0], qraw[rb][s][1]);
+      } else {
+        qraw[rb][s][0] = *reinterpret_cast<const u32x2*>(qrow + t0);
+        qraw[rb][s][1] = *reinterpret_cast<const u32x2*>(qrow + D / 2 + t0);
       }
     }
   }
-  // Eight-wave and two-block workgroups keep the loader's per-row angle constants in registers.
-  PLoader<D, KMI, NT, RB == 2 || NW == 8> ld;
-  ld.init(tid);
-  TileIter<kSub> it;
-  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
-  bool have = it.seek(a.causal, qmax);
-  if (have)
-    ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
-             min(kSub, it.cur.len - it.j0));
-
-  if (!ALIBI && tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
-  __syncthreads();
+  // Every table entry this thread computes below is for pair t = tid % (D/2) (the block size is a multiple of D/2):
+  // each thread evaluates its own frequency, with no barrier before the tables.  The per-tile bases in the loop read
+  // the frequencies from LDS (fewer registers held across the loop); the tables' barrier publishes them.
+  const double rev = ALIBI ? 0.0 : theta_rev(tid % (D / 2), D, a.rope_log2_base, a.inv_freq);
+  if (tid < D / 2) sm.freq[tid] = rev;
 
   // Angle tables: per-row deltas cos/sin(delta theta_t), delta < 32 (queries and keys), and the query block bases
   // cos/sin(32 a theta_t), a = qmin / 32 .. qmax / 32.
   const int qa0 = qmin / kAngleRows, nqb = qmax / kAngleRows - qa0 + 1;
+  static_assert(NT % (D / 2) == 0, "a thread's table entries share one pair index");
   for (int e = tid; e < (ALIBI ? 0 : (kAngleRows + nqb) * (D / 2)); e += NT) {
     const int trow = e / (D / 2), t = e % (D / 2);
     float* dst = trow < kAngleRows ? sm.csd + trow * S::CSD_LD : sm.qb[trow - kAngleRows];
     const int p = trow < kAngleRows ? trow : kAngleRows * (qa0 + trow - kAngleRows);
-    *reinterpret_cast<float2*>(dst + cs_idx<D>(t)) = rope_cs(p, sm.freq[t]);
+    *reinterpret_cast<float2*>(dst + cs_idx<D>(t)) = rope_cs(p, rev);
   }
   __syncthreads();
+
+  // The chunk-table walk (its loads have been in flight during the tables) and the first tile's K / V, whose
+  // latency the Q rotation below covers.
+  // Eight-wave and two-block workgroups keep the loader's per-row angle constants in registers.
+  PLoader<D, KMI, NT, RB == 2 || NW == 8> ld;
+  ld.init(tid);
+  TileIter<kSub> it;
+  it.init(a.chunks, c0, c1, split, a.splits, first);
+  bool have = it.seek(a.causal, qmax);
+  if (have)
+    ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+             min(kSub, it.cur.len - it.j0));
 
   // Pre-rotated queries take the angle row of position 0 (cos 1, sin 0) for both parts, which leaves them exactly
   // as given without a second code path.
@@ -787,7 +819,9 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     const float* qdr = sm.csd + (a.q_prerot ? 0 : qpos[rb] & (kAngleRows - 1)) * S::CSD_LD;
 #pragma unroll
     for (int s = 0; s < D / 16; ++s)
-      qf[rb][s] = ALIBI ? as_bf16x8(u32x4{qraw[rb][s][0][0], qraw[rb][s][0][1], qraw[rb][s][1][0], qraw[rb][s][1][1]})
+      qf[rb][s] = ALIBI ? as_bf16x8(rvalid[rb] ? u32x4{qraw[rb][s][0][0], qraw[rb][s][0][1], qraw[rb][s][1][0],
+                                                       qraw[rb][s][1][1]}
+                                             : u32x4{0, 0, 0, 0})
                         : q_fragment_tab<D>(qraw[rb][s][0], qraw[rb][s][1], 8 * s + 4 * h2, qbr, qdr, rvalid[rb]);
   }
 

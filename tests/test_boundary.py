@@ -189,6 +189,22 @@ def test_workspace_size_matches_split_formula(ops):
     assert ops.decode_workspace_size(auto, 0, 100) == 0
 
 
+def test_prefill_xcd_map_choice(ops):
+    """The interleaved XCD map applies to ragged batches (mean query length under 3/4 of the maximum) whose
+    batch x splits is a multiple of 8; the prefill parity case varlen_g7_b8 is built to take it."""
+    w = W.varlen_rag(seed=30, batch=8, hq=28, hkv=4, d=128, pool_chunks=10, len_lo=40, len_hi=300, k_lo=2, k_hi=4,
+                     q_lo=10, q_hi=90)
+    cfg = ops.config_of(w)
+    assert 4 * w.total_q < 3 * w.batch * w.max_q_len
+    per_split = w.total_q * w.num_q_heads * (2 * w.head_dim + 4)
+    n = ops.prefill_workspace_size(cfg, w.batch, w.total_q, w.max_q_len, w.max_kv_len)
+    splits = max(1, n // per_split)
+    assert n == (0 if splits == 1 else splits * per_split)
+    assert (w.batch * splits) % 8 == 0 and splits >= 2
+    # several query tiles per KV head (256-row tiles at head_dim 128) and a ragged tail
+    assert w.max_q_len * (w.num_q_heads // w.num_kv_heads) > 256
+
+
 def test_strerror_and_version(ops):
     assert ops.strerror(0) == "success"
     assert "workspace" in ops.strerror(-3)

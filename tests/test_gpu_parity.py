@@ -110,6 +110,9 @@ PREFILL_CASES = {
                                      k_lo=2, k_hi=5, q_lo=1, q_hi=40), {}),
     "varlen_g8_d64": (W.varlen_rag, dict(seed=15, batch=3, hq=16, hkv=2, d=64, pool_chunks=8, len_lo=30,
                                          len_hi=300, k_lo=1, k_hi=4, q_lo=20, q_hi=70), dict(num_splits=2)),
+    # ragged batch of 8: batch x splits is a multiple of 8, so the workgroups take the interleaved XCD map
+    "varlen_g7_b8": (W.varlen_rag, dict(seed=30, batch=8, hq=28, hkv=4, d=128, pool_chunks=10, len_lo=40,
+                                        len_hi=300, k_lo=2, k_hi=4, q_lo=10, q_hi=90), {}),
     "icl_small": (W.icl_prefill, dict(seed=16, batch=2, hq=8, hkv=2, d=128, n_chunks=12, chunk_len=32, q_len=80,
                                       decode_steps=4), {}),
 }
@@ -301,7 +304,8 @@ def test_full_size_sampled(name):
 LOCAL = dict(key_positions=ops.KEYS_LOCAL)
 
 
-@pytest.mark.parametrize("name", ["rag_d128_g4", "rag_d64_g2_split3", "rag_d128_g1_split1", "varlen_g7", "icl_small"])
+@pytest.mark.parametrize("name", ["rag_d128_g4", "rag_d64_g2_split3", "rag_d128_g1_split1", "varlen_g7",
+                                  "varlen_g7_b8", "icl_small"])
 def test_local_key_store_prefill_matches_oracle(name):
     fn, kw, ckw = PREFILL_CASES[name]
     run_and_check(fn(**kw), "local " + name, {**ckw, **LOCAL})
