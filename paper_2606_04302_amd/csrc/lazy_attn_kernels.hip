@@ -418,14 +418,13 @@ __device__ __forceinline__ const uint16_t* v_ptr(const uint16_t* pool, const Rec
 //    and unit z runs on XCD z % 8 (its XCD's m-th workgroup is tile m % (nx ny) of unit z = L % 8 + 8 (m / (nx ny))),
 //    so requests of different lengths are spread evenly over the XCDs instead of piling onto some of them.
 // Both fall back to the identity where the counts do not divide by 8.
+// Both maps are evaluated and one is selected, with no branch: the kernel's first loads then issue together.
 __device__ __forceinline__ int xcd_remap(int id, int n, int inner, int units, bool interleave) {
-  if (interleave) {
-    if (units & 7) return id;
-    const int m = id >> 3;
-    return m % inner + inner * ((id & 7) + 8 * (m / inner));
-  }
+  const int m = id >> 3;
+  const int spread = (units & 7) ? id : m % inner + inner * ((id & 7) + 8 * (m / inner));
   const int per = n >> 3;
-  return id < (per << 3) ? (id & 7) * per + (id >> 3) : id;
+  const int whole = id < (per << 3) ? (id & 7) * per + m : id;
+  return interleave ? spread : whole;
 }
 
 // Query positions of a workgroup of at most 256 rows span at most 256 consecutive positions: at most 9 blocks of 32.
@@ -732,18 +731,25 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   constexpr int BM = 32 * NW * RB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nx = gridDim.x, ny = gridDim.y;
+  // The argument block's lines are fetched in one round trip: the index arithmetic below needs the grid constants and
+  // the split count, and right after it the index-array pointers (otherwise loaded one round trip later).
+  asm volatile("" ::"s"(a.q_start), "s"(a.chunk_start), "s"(a.splits), "s"(a.xcd_interleave), "s"(nx), "s"(ny),
+               "s"(gridDim.z));
   const int lid = uniform(xcd_remap(blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z), nx * ny * gridDim.z, nx * ny,
                                     gridDim.z, a.xcd_interleave != 0));
   const int qtile = lid % nx;
   const int g = (lid / nx) % ny;
   const int zz = lid / (nx * ny);
   const int r = zz / a.splits, split = zz % a.splits;
-  const int qs = as_const(a.q_start)[r], qe = as_const(a.q_start)[r + 1];
+  // The request's index entries are loaded together, before the exit test that needs only q_start (the empty asm
+  // keeps the compiler from sinking the other loads below the test, which would cost two more round trips).
+  const int qs = as_const(a.q_start)[r], qe = as_const(a.q_start)[r + 1], qp0 = as_const(a.q_pos0)[r];
+  const int c0 = as_const(a.chunk_start)[r], c1 = as_const(a.chunk_start)[r + 1];
+  asm volatile("" ::"s"(qp0), "s"(c0), "s"(c1));
   const int G = a.group;
   const int nrows = (qe - qs) * G;
   const int row0 = qtile * BM;
   if (row0 >= nrows) return;
-  const int qp0 = as_const(a.q_pos0)[r];
 
   const int h2 = lane >> 5;
   bool rvalid[RB];
@@ -761,7 +767,6 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
 
   // Loads first: the first block of the chunk table and raw Q.  The angle tables below need neither and are computed
   // while they are in flight.
-  const int c0 = as_const(a.chunk_start)[r], c1 = as_const(a.chunk_start)[r + 1];
   const TileIter<kSub>::First first = TileIter<kSub>::first_block(a.chunks, c0, c1);
   u32x2 qraw[RB][D / 16][2];
 #pragma unroll
