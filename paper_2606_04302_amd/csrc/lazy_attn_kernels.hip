@@ -1155,30 +1155,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int hcount = min(kDecodeHeadsPerGroup, G - kDecodeHeadsPerGroup * hg);
   const int col = lane & 15, kq = lane >> 4;
   const int qpos = as_const(a.q_pos0)[r];
+  const int c0 = as_const(a.chunk_start)[r], c1 = as_const(a.chunk_start)[r + 1];
+  asm volatile("" ::"s"(qpos), "s"(c0), "s"(c1));  // one round trip for the three (the compiler would sink qpos)
 
   const bool hvalid = col < hcount;
   const int head = g * G + kDecodeHeadsPerGroup * hg + (hvalid ? col : 0);
-  // Raw Q first, then the chunk-table walk and the first tile's K / V: the tables and the Q rotation below are
-  // computed while those loads are in flight (Q, issued first, is waited for without waiting for the tile).
+  // Loads first: the first chunk-table block and the raw Q (columns past the group's heads read a valid head and
+  // are zeroed once Q is needed; no load sits behind a per-lane branch, which would make the compiler wait for
+  // every load in flight at its first use).  The frequency and per-row tables are built while they are in flight,
+  // then the table walk issues this wave's first tile.
+  const TileIter<kDecWaveKeys>::First first = TileIter<kDecWaveKeys>::first_block(a.chunks, c0, c1);
   u32x4 qraw[SP][2];
   {
     const uint16_t* qrow = a.q + ((int64_t)r * a.hq + head) * D;
 #pragma unroll
-    for (int s = 0; s < SP; ++s) {
-      qraw[s][0] = qraw[s][1] = u32x4{0, 0, 0, 0};
-      if (hvalid) dec_k_pairs<D, IL>(qrow, s, kq, qraw[s][0], qraw[s][1]);
-    }
+    for (int s = 0; s < SP; ++s) dec_k_pairs<D, IL>(qrow, s, kq, qraw[s][0], qraw[s][1]);
   }
-  // This wave's tiles: every fourth tile of the split, starting at tile `wave`.
-  TileIter<kDecWaveKeys> it;
-  it.init(a.chunks, as_const(a.chunk_start)[r], as_const(a.chunk_start)[r + 1], split, a.splits);
-  for (int k = 0; k < wave && it.left > 0; ++k) it.step();
-  bool have = it.seek(a.causal, qpos);
-  DecTile<D> cur, nxt;
-  if (have)
-    dec_fetch<D, IL>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
-                 min(kDecWaveKeys, it.cur.len - it.j0), lane);
-
   if (!ALIBI && tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
   __syncthreads();
   if (ROT) {
@@ -1187,8 +1179,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       const int dr = e / (D / 2), t = e % (D / 2);
       *reinterpret_cast<float2*>(sm.csd + dec_row<D>(dr) + 2 * t) = rope_cs(dr, sm.freq[t]);
     }
-    if (have && lane < D / 2)
-      *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
+  }
+  // This wave's tiles: every fourth tile of the split, starting at tile `wave`.
+  TileIter<kDecWaveKeys> it;
+  it.init(a.chunks, c0, c1, split, a.splits, first);
+  for (int k = 0; k < wave && it.left > 0; ++k) it.step();
+  bool have = it.seek(a.causal, qpos);
+  DecTile<D> cur, nxt;
+  if (have)
+    dec_fetch<D, IL>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+                 min(kDecWaveKeys, it.cur.len - it.j0), lane);
+  if (ROT && have && lane < D / 2)
+    *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
+#pragma unroll
+  for (int s = 0; s < SP; ++s) {
+    const u32x4 zero = {0, 0, 0, 0};
+    qraw[s][0] = hvalid ? qraw[s][0] : zero;
+    qraw[s][1] = hvalid ? qraw[s][1] : zero;
   }
   // Q fragments in the decode head-dimension order, rotated at the query position.  With local-position keys they
   // are built per record instead (below), from the raw query.
