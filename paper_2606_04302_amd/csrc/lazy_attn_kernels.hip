@@ -1552,7 +1552,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __res
                                                            uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int TPR = D / 8;
   constexpr int LPR = TPR * CG;        // lanes per row
-  constexpr int U = CG == 1 ? 4 : 2;   // splits loaded together per lane
+  constexpr int U = 4;                 // splits loaded together per lane: up to 4 CG splits per round trip
   static_assert(LPR <= 64 && 64 % LPR == 0, "a row's lanes lie in one wave");
   const int row = blockIdx.x * (kThreads / LPR) + threadIdx.x / LPR;
   const int d8 = threadIdx.x % TPR;
@@ -1563,12 +1563,12 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __res
   if (live && slot_start) splits = slot_start[row / hq + 1] - slot_start[row / hq];
   float mmax = -INFINITY;
   if (live) {
-    for (int s0 = 0; s0 < splits; s0 += 8) {
-      float l[8];
+    for (int s0 = 0; s0 < splits; s0 += 16) {  // 16 log-sum-exps per round trip
+      float l[16];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) l[e] = s0 + e < splits ? part_lse[(int64_t)(s0 + e) * rows + row] : -INFINITY;
+      for (int e = 0; e < 16; ++e) l[e] = s0 + e < splits ? part_lse[(int64_t)(s0 + e) * rows + row] : -INFINITY;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) mmax = fmaxf(mmax, l[e]);
+      for (int e = 0; e < 16; ++e) mmax = fmaxf(mmax, l[e]);
     }
   }
   float den = 0.f, sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
