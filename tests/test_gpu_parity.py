@@ -475,6 +475,30 @@ def test_shared_decode_full_size_sampled(paged):
     assert_close(out, None, ref_o, ref_l, rows, tag=f"shared full rag_decode {'paged64' if paged else ''}")
 
 
+def _long_tables(seed, kind, n_records):
+    """Requests of many short records (1..12 keys, contiguous positions): the tile walk counts tiles 256 records at a
+    time and finds a split's first record 64 records at a time, so tables longer than 256 records take the paths
+    past the first block."""
+    rng = np.random.default_rng(seed)
+    reqs = []
+    for n in n_records:
+        lens = rng.integers(1, 13, size=n)
+        pos = np.concatenate([[0], np.cumsum(lens)[:-1]])
+        q_len = 1 if kind == "decode" else 5
+        reqs.append(dict(chunks=[(int(a), int(b)) for a, b in zip(lens, pos)], q_len=q_len,
+                         q_pos0=int(pos[-1] + lens[-1]) - (q_len - 1 if kind == "decode" else 0)))
+    return W.custom(seed, 8, 2, 128, 1e4, reqs, kind=kind)
+
+
+@pytest.mark.parametrize("kind", ["prefill", "decode"])
+@pytest.mark.parametrize("splits", [0, 5])
+def test_long_chunk_tables(kind, splits):
+    w = _long_tables(140 + splits, kind, [300, 700, 64])
+    ckw = dict(num_splits=splits) if splits else {}
+    run_and_check(w, f"{kind} long tables splits={splits}", ckw)
+    run_and_check(w, f"{kind} long tables splits={splits} local", {**ckw, **LOCAL})
+
+
 # --------------------------------------------------------------------------------------------------------------
 # Paged (block-granular) stores: each chunk's K/V in fixed-size blocks scattered over the pool, one record per
 # block.  The kernels see ordinary records (tiles never straddle a record); block sizes below a tile exercise the
