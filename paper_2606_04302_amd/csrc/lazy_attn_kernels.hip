@@ -33,6 +33,7 @@
 // in which P leaves the S^T accumulators, so P needs no shuffling.
 #include <hip/hip_runtime.h>
 #include <math.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include "lazy_attn_internal.h"
@@ -899,6 +900,45 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
     have = have_next;
   }
 
+  if constexpr (NBUF == 2 && RB == 1) {
+    // Normalised output and log-sum-exp: the final result, or with several splits this split's partial result.
+    // The output goes through LDS (the tile buffers are free after the loop's last barrier): each wave stages its 32
+    // rows, then writes whole 256-byte rows, 16 bytes per lane, so that one store instruction covers four rows
+    // instead of 16 bytes in each of 32 rows.
+    constexpr int OLD = D + 8;
+    using SM = PrefillSmem<D, NBUF>;
+    static_assert(offsetof(SM, v) == sizeof(sm.k) &&
+                      sizeof(sm.k) + sizeof(sm.v) >= sizeof(uint16_t) * NW * 32 * OLD,
+                  "the output stage spans the K and V tile buffers");
+    uint16_t* stage = &sm.k[0][0] + wave * 32 * OLD;
+    const float ltot = xor32_sum(lsum[0]);
+    const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+        *reinterpret_cast<u32x2*>(stage + (lane & 31) * OLD + 32 * db + 8 * q4 + 4 * h2) =
+            u32x2{pack2(o[0][db][4 * q4] * inv, o[0][db][4 * q4 + 1] * inv),
+                  pack2(o[0][db][4 * q4 + 2] * inv, o[0][db][4 * q4 + 3] * inv)};
+    if (rvalid[0] && h2 == 0) {
+      const int64_t orow = (int64_t)(qs + tok[0]) * a.hq + head[0];
+      float* lse_dst = a.splits == 1 ? (a.lse ? a.lse + orow : nullptr) : a.ws_lse + (int64_t)split * a.total_q * a.hq + orow;
+      if (lse_dst) *lse_dst = ltot > 0.f ? (m2[0] + log2f(ltot)) * kLn2 : -INFINITY;
+    }
+    __syncthreads();
+    uint16_t* base = a.splits == 1 ? a.out : a.ws_o + (int64_t)split * a.total_q * a.hq * D;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int lrow = 4 * i + (lane >> 4);
+      const int prow = row0 + 32 * wave + lrow;
+      if (prow < nrows) {
+        const int64_t orow = (int64_t)(qs + prow / G) * a.hq + g * G + prow % G;
+        *reinterpret_cast<u32x4*>(base + orow * D + 8 * (lane & 15)) =
+            *reinterpret_cast<const u32x4*>(stage + lrow * OLD + 8 * (lane & 15));
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const float ltot = xor32_sum(lsum[rb]);
