@@ -115,6 +115,10 @@ PREFILL_CASES = {
                                         len_hi=300, k_lo=2, k_hi=4, q_lo=10, q_hi=90), {}),
     "icl_small": (W.icl_prefill, dict(seed=16, batch=2, hq=8, hkv=2, d=128, n_chunks=12, chunk_len=32, q_len=80,
                                       decode_steps=4), {}),
+    # eight-wave workgroups (80 x 4 = 320 packed rows: a full and a partial row tile) writing the final output and
+    # log-sum-exp directly (one split)
+    "icl_small_split1": (W.icl_prefill, dict(seed=17, batch=2, hq=8, hkv=2, d=128, n_chunks=12, chunk_len=32, q_len=80,
+                                             decode_steps=4), dict(num_splits=1)),
 }
 
 
@@ -305,7 +309,7 @@ LOCAL = dict(key_positions=ops.KEYS_LOCAL)
 
 
 @pytest.mark.parametrize("name", ["rag_d128_g4", "rag_d64_g2_split3", "rag_d128_g1_split1", "varlen_g7",
-                                  "varlen_g7_b8", "icl_small"])
+                                  "varlen_g7_b8", "icl_small", "icl_small_split1"])
 def test_local_key_store_prefill_matches_oracle(name):
     fn, kw, ckw = PREFILL_CASES[name]
     run_and_check(fn(**kw), "local " + name, {**ckw, **LOCAL})
