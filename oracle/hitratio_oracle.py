@@ -9,6 +9,11 @@ TEST INFRASTRUCTURE ONLY (like lazy_oracle): only the tests call it; it shares n
 - ``zipf_mass``: the hit ratio of a static cache of the top C of N documents (H_agnostic of the same passage).
 - ``lru``: a textbook least-recently-used cache written with an ordered dict, returning the hit / eviction
   sequence of a key trace.
+
+Pins (tests/test_hitsim.py): the analytic model reproduces the paper's printed 2.86x and the alpha = 0 and alpha = 1
+closed forms; ``lru`` reproduces hand-derived eviction sequences (tests/golden/lru_traces.json, chosen so that FIFO
+or MRU replacement gives different ones) and, on long independent Zipf traces, Che's approximation of the LRU hit
+ratio, below the static top-C bound ``zipf_mass``, which a sampled static cache matches.
 """
 from __future__ import annotations
 
