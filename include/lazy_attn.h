@@ -321,6 +321,26 @@ LAZY_API int lazy_attn_validate(const lazy_attn_params_t* params, const int32_t*
                        const lazy_chunk_t* chunks, const int32_t* chunk_start, int32_t batch, int64_t k_pool_elems,
                        int64_t v_pool_elems, int64_t* bad_index, const char** reason);
 
+/*
+ * Host-side check of a shared-decode plan (HOST copies of what lazy_attn_decode_shared would read; CPU only).  The
+ * kernel trusts these tables, so a plan built by hand rather than by lazy_shared_decode_plan should pass this first.
+ * Checks: slot_start starts at 0, is non-decreasing and no request has more than max_slots slots; every range has
+ * non-negative 16-byte-aligned offsets, 0 <= key_begin < key_end <= both strides and its K / V inside the pools
+ * (pool sizes in elements); every item has 1..LAZY_SHARED_MAX_RANGES ranges inside the range table (exactly one
+ * with LAZY_KEYS_LOCAL), all but the last of range_keys keys (a multiple of 32 when there are several), the last
+ * 1..range_keys keys, 1..floor(16 / G) users inside the user table and reserved = 0; every user names a request of
+ * the batch, one of its slots and key positions in 0..LAZY_MAX_POS; every slot of every request is written by
+ * exactly one (item, user) pair.  q_pos (nullable) must lie in 0..LAZY_MAX_POS - 1.  Returns LAZY_OK, LAZY_EDATA
+ * (with the offending item / range / request index in *bad_index and a reason), LAZY_EINVAL for bad arguments or
+ * LAZY_EUNSUPPORTED for a head layout the shared decode does not take.
+ */
+LAZY_API int lazy_shared_decode_validate(const lazy_attn_params_t* params, const lazy_shared_item_t* items,
+                                         int32_t num_items, const lazy_shared_range_t* ranges, int32_t num_ranges,
+                                         const lazy_shared_user_t* users, int32_t num_users,
+                                         const int32_t* slot_start, int32_t batch, int32_t max_slots,
+                                         const int32_t* q_pos, int64_t k_pool_elems, int64_t v_pool_elems,
+                                         int64_t* bad_index, const char** reason);
+
 /* Static text for a LAZY_* code. */
 LAZY_API const char* lazy_attn_strerror(int code);
 

@@ -327,6 +327,20 @@ struct TileIter {
     }
     return false;
   }
+  // Advance by `n` tiles (fewer if the split ends first).
+  __device__ void skip(int n) {
+    for (int k = 0; k < n && left > 0; ++k) step();
+  }
+  // seek() for a walker that owns every stride-th tile of the split (the decode waves): invisible tiles are passed
+  // over `stride` at a time, so the walker stays on its own residue class of tiles.  Positions need not increase
+  // along the table, so a tile after the query may precede visible ones.
+  __device__ bool seek_strided(bool causal, int qmax, int stride) {
+    while (left > 0) {
+      if (!causal || cur.pos + j0 <= qmax) return true;
+      skip(stride);
+    }
+    return false;
+  }
 };
 
 // Angles: the rotation of key j of a chunk (position pos + j) uses one decomposition everywhere (lazy kernels and
@@ -1223,8 +1237,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // This wave's tiles: every fourth tile of the split, starting at tile `wave`.
   TileIter<kDecWaveKeys> it;
   it.init(a.chunks, c0, c1, split, a.splits, first);
-  for (int k = 0; k < wave && it.left > 0; ++k) it.step();
-  bool have = it.seek(a.causal, qpos);
+  it.skip(wave);
+  bool have = it.seek_strided(a.causal, qpos, 4);
   DecTile<D> cur, nxt;
   if (have)
     dec_fetch<D, IL>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
@@ -1319,8 +1333,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             as_bf16x8(u32x4{pack2(y2[0], y2[1]), pack2(y2[2], y2[3]), pack2(y2[4], y2[5]), pack2(y2[6], y2[7])});
       }
     }
-    for (int k = 0; k < 4 && it.left > 0; ++k) it.step();
-    const bool have_next = it.seek(a.causal, qpos);
+    it.skip(4);
+    const bool have_next = it.seek_strided(a.causal, qpos, 4);
     if (have_next) {
       dec_fetch<D, IL>(nxt, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
                    min(kDecWaveKeys, it.cur.len - it.j0), lane);
@@ -1419,14 +1433,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   __shared__ lazy_shared_range_t srg[LAZY_SHARED_MAX_RANGES];
   const cptr<lazy_shared_item_t> item = as_const(a.items) + blockIdx.x;
   const int g = blockIdx.y;
-  // Item fields come from the planner; the clamps keep the LDS range table in bounds for any values.
+  // Item fields come from the planner (lazy_shared_decode_validate checks a plan on the host).  The clamps keep
+  // every LDS index in bounds whatever the item holds: the range table (at most LAZY_SHARED_MAX_RANGES entries) and
+  // the per-user angle rows (at most floor(16 / G) users, one MFMA column per (user, query head)).
+  const int G = a.group;
   const int rb = item->range_begin, nr = max(1, min(item->num_ranges, LAZY_SHARED_MAX_RANGES));
   const int rk = max(1, item->range_keys);
-  const int u0 = item->user_begin, nu = item->num_users;
+  const int u0 = item->user_begin, nu = max(0, min(item->num_users, 16 / G));
+  if (nu == 0) return;  // no user: nothing to score or write (the whole workgroup leaves before any barrier)
   const cptr<lazy_shared_range_t> rgs = as_const(a.ranges) + rb;
   const int nk = (nr - 1) * rk + (rgs[nr - 1].key_end - rgs[nr - 1].key_begin);  // keys of the run
   if (tid < nr) srg[tid] = a.ranges[rb + tid];
-  const int G = a.group;
   const int col = lane & 15, kq = lane >> 4;
   const int cu = col / G;
   const bool cvalid = cu < nu;

@@ -77,6 +77,9 @@ SIGNATURES = {
     "lazy_attn_decode_shared": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_p,
                                          _c_p, _c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_sz, _c_p]),
     "lazy_attn_decode_shared_workspace_size": (_c_sz, [ctypes.POINTER(LazyAttnParams), _c_i32, _c_i32]),
+    "lazy_shared_decode_validate": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_i32, _c_p, _c_i32, _c_p,
+                                             _c_i32, _c_p, _c_i32, _c_i32, _c_p, _c_i64, _c_i64,
+                                             ctypes.POINTER(_c_i64), ctypes.POINTER(ctypes.c_char_p)]),
     "lazy_pool_create": (_c_p, [_c_i32]),
     "lazy_pool_destroy": (None, [_c_p]),
     "lazy_pool_acquire": (_c_i32, [_c_p, ctypes.c_uint64, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32),
@@ -367,6 +370,26 @@ def shared_decode_plan(cfg: Config, chunks: np.ndarray, chunk_start, max_keys_pe
         return SharedPlan(items[: n_items.value].copy(), ranges[: n_ranges.value].copy(), users[: n_users.value].copy(),
                           slot_start)
     raise RuntimeError("lazy_shared_decode_plan: capacity did not converge")
+
+
+def validate_shared_plan(cfg: Config, plan: SharedPlan, q_pos, k_pool_elems: int, v_pool_elems: int,
+                         max_slots: int | None = None):
+    """lazy_shared_decode_validate on a host plan.  Returns (code, bad_index, reason)."""
+    items = np.ascontiguousarray(plan.items, dtype=ITEM_DTYPE)
+    ranges = np.ascontiguousarray(plan.ranges, dtype=RANGE_DTYPE)
+    users = np.ascontiguousarray(plan.users, dtype=USER_DTYPE)
+    ss = np.ascontiguousarray(plan.slot_start, dtype=np.int32)
+    qp = None if q_pos is None else np.ascontiguousarray(q_pos, dtype=np.int32)
+    bad = _c_i64(-1)
+    why = ctypes.c_char_p()
+    p = cfg.c()
+    ptr = lambda a: a.ctypes.data if a.size else None
+    code = lib().lazy_shared_decode_validate(ctypes.byref(p), ptr(items), items.size, ptr(ranges), ranges.size,
+                                             ptr(users), users.size, ss.ctypes.data, ss.size - 1,
+                                             plan.max_slots if max_slots is None else max_slots,
+                                             None if qp is None else qp.ctypes.data, k_pool_elems, v_pool_elems,
+                                             ctypes.byref(bad), ctypes.byref(why))
+    return code, int(bad.value), (why.value or b"").decode()
 
 
 @dataclass

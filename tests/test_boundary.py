@@ -443,7 +443,7 @@ int main() {
   lazy_attn_params_t p = {8, 2, 128, 1, 1e4f, 0.f, nullptr, 0, 0};
   // 3 requests; records 0/2/4 read the same stored chunk at different offsets, one 2500-key private record, and a
   // paged run (64-key blocks 5..7 then 8..9) that requests 1 and 2 both read
-  std::vector<lazy_chunk_t> c = {{0, 4096, 300, 0, 300, 300}, {9000, 9500, 20, 300, 32, 32},
+  std::vector<lazy_chunk_t> c = {{0, 4096, 300, 0, 300, 300}, {9000, 9504, 20, 300, 32, 32},
                                  {0, 4096, 300, 50, 300, 300}, {20000, 90000, 2500, 0, 2500, 2500},
                                  {0, 4096, 300, 7, 300, 300},
                                  {100000, 200000, 64, 3000, 64, 64}, {101000, 201000, 64, 3064, 64, 64},
@@ -467,6 +467,27 @@ int main() {
         code = lazy_shared_decode_plan(&p, c.data(), table, 3, step, items.data(), ni, ranges.data(), nr,
                                        users.data(), nu, &ni, &nr, &nu, ss);
         if (code != LAZY_OK || ss[0] != 0 || ss[3] > nu) ++fails;
+        int32_t ms = 0;
+        for (int r = 0; r < 3; ++r) ms = ss[r + 1] - ss[r] > ms ? ss[r + 1] - ss[r] : ms;
+        int64_t bad; const char* why;
+        int32_t qpos[3] = {5000, 5000, 5000};
+        if (lazy_shared_decode_validate(&p, items.data(), ni, ranges.data(), nr, users.data(), nu, ss, 3, ms, qpos,
+                                        1 << 20, 1 << 20, &bad, &why) != LAZY_OK) {
+          printf("plan rejected: %s\n", why);
+          ++fails;
+        }
+        if (ni > 0) {  // an item with too many users is rejected, and the validator stays in bounds doing so
+          std::vector<lazy_shared_item_t> m = items;
+          m[0].num_users = 1000;
+          if (lazy_shared_decode_validate(&p, m.data(), ni, ranges.data(), nr, users.data(), nu, ss, 3, ms, qpos,
+                                          1 << 20, 1 << 20, &bad, &why) != LAZY_EDATA)
+            ++fails;
+          m = items;
+          m[0].range_begin = nr;
+          if (lazy_shared_decode_validate(&p, m.data(), ni, ranges.data(), nr, users.data(), nu, ss, 3, ms, qpos,
+                                          1 << 20, 1 << 20, &bad, &why) != LAZY_EDATA)
+            ++fails;
+        }
         for (const auto& it : items) {
           if (it.user_begin < 0 || it.user_begin + it.num_users > nu || it.num_users < 1 || it.num_users > 4) ++fails;
           if (it.range_begin < 0 || it.num_ranges < 1 || it.range_begin + it.num_ranges > nr) ++fails;
@@ -487,8 +508,88 @@ int main() {
 """)
     exe = tmp_path / "plan_drv"
     subprocess.run(["g++", "-std=c++17", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-I",
-                    os.path.join(ROOT, "include"), str(drv), os.path.join(B.CSRC, "lazy_attn_plan.cpp"), "-o",
+                    os.path.join(ROOT, "include"), str(drv), os.path.join(B.CSRC, "lazy_attn_plan.cpp"),
+                    os.path.join(B.CSRC, "lazy_attn_validate.cpp"), "-o",
                     str(exe)], check=True)
     res = subprocess.run([str(exe)], capture_output=True, text=True)
     assert res.returncode == 0, res.stdout + res.stderr
     assert "ok=1" in res.stdout
+
+
+# ---------------------------------------------------------------------------------------------------------------
+# Host check of shared-decode plans (the kernel trusts its item / range / user tables).
+# ---------------------------------------------------------------------------------------------------------------
+def _plan_case(ops, local=False, paged=0):
+    w = W.rag_decode(seed=9, batch=7, hq=8, hkv=2, n_chunks=4, chunk_len=300, pool_chunks=6, tail_len=40,
+                     tail_cap=100)
+    if paged:
+        w = W.paginate(w, paged, seed=1)
+    cfg = ops.config_of(w, **({"key_positions": ops.KEYS_LOCAL} if local else {}))
+    return w, cfg, ops.shared_decode_plan(cfg, w.chunks, w.chunk_start, 0)
+
+
+@pytest.mark.parametrize("local,paged", [(False, 0), (True, 0), (False, 64), (True, 32)])
+def test_shared_plan_validator_accepts_planner_output(ops, local, paged):
+    w, cfg, plan = _plan_case(ops, local, paged)
+    code, bad, why = ops.validate_shared_plan(cfg, plan, w.q_pos0, w.pool.size, w.pool.size)
+    assert code == ops.LAZY_OK, (bad, why)
+
+
+def _mut(field, idx, value, table="items"):
+    def f(plan):
+        getattr(plan, table)[field][idx] = value
+    return f
+
+
+SHARED_PLAN_MUTATIONS = [
+    (_mut("num_users", 0, 5), "num_users"),            # G = 4: at most 4 users per item
+    (_mut("num_users", 0, 0), "num_users"),
+    (_mut("num_ranges", 0, 0), "num_ranges"),
+    (_mut("num_ranges", 0, 65), "num_ranges"),
+    (_mut("range_begin", 0, -1), "ranges outside"),
+    (_mut("user_begin", 0, 10 ** 6), "users outside"),
+    (_mut("reserved", 0, 1), "reserved"),
+    (_mut("range_keys", 0, 0), "range_keys"),
+    (_mut("k_offset", 0, 3, "ranges"), "multiples of 8"),
+    (_mut("key_end", 0, 10 ** 6, "ranges"), "stride"),
+    (_mut("key_begin", 0, -2, "ranges"), "non-empty"),
+    (_mut("request", 0, 99, "users"), "request out of range"),
+    (_mut("slot", 0, 50, "users"), "slot out of range"),
+    (_mut("pos_offset", 0, -5, "users"), "positions out of range"),
+]
+
+
+@pytest.mark.parametrize("mutate,reason", SHARED_PLAN_MUTATIONS)
+def test_shared_plan_validator_rejects_contract_violations(ops, mutate, reason):
+    w, cfg, plan = _plan_case(ops)
+    mutate(plan)
+    code, bad, why = ops.validate_shared_plan(cfg, plan, w.q_pos0, w.pool.size, w.pool.size)
+    assert code == ops.LAZY_EDATA and reason in why, (code, why)
+
+
+def test_shared_plan_validator_slot_coverage_pools_and_args(ops):
+    w, cfg, plan = _plan_case(ops)
+    # a slot written twice (and another never): two users of different items pointed at one slot
+    p2 = ops.SharedPlan(plan.items.copy(), plan.ranges.copy(), plan.users.copy(), plan.slot_start.copy())
+    r = int(p2.users["request"][0])
+    same = np.nonzero(p2.users["request"] == r)[0]
+    p2.users["slot"][same[1]] = p2.users["slot"][same[0]]
+    code, _, why = ops.validate_shared_plan(cfg, p2, w.q_pos0, w.pool.size, w.pool.size)
+    assert code == ops.LAZY_EDATA and "exactly once" in why
+    # pools too small, too few slots allowed, a local-position store with multi-range items, bad query position
+    assert ops.validate_shared_plan(cfg, plan, w.q_pos0, 1024, w.pool.size)[2] == "range K outside the pool"
+    assert ops.validate_shared_plan(cfg, plan, w.q_pos0, w.pool.size, 1024)[2] == "range V outside the pool"
+    assert "max_slots" in ops.validate_shared_plan(cfg, plan, w.q_pos0, w.pool.size, w.pool.size, max_slots=1)[2]
+    wp, cp, pp = _plan_case(ops, False, 64)
+    assert pp.items["num_ranges"].max() > 1
+    local = ops.config_of(wp, key_positions=ops.KEYS_LOCAL)
+    assert "single ranges" in ops.validate_shared_plan(local, pp, wp.q_pos0, wp.pool.size, wp.pool.size)[2]
+    qp = np.array(w.q_pos0, dtype=np.int32)
+    qp[2] = -1
+    assert "query position" in ops.validate_shared_plan(cfg, plan, qp, w.pool.size, w.pool.size)[2]
+    # G = 17 is outside what the shared decode takes; a null parameter block is an argument error
+    assert ops.validate_shared_plan(ops.Config(34, 2, 128, 1e4), plan, None, w.pool.size,
+                                    w.pool.size)[0] == ops.LAZY_EUNSUPPORTED
+    L = ops.lib()
+    assert L.lazy_shared_decode_validate(None, None, 0, None, 0, None, 0, plan.slot_start.ctypes.data, 0, 0, None,
+                                         0, 0, None, None) == ops.LAZY_EINVAL
