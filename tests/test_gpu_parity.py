@@ -289,15 +289,16 @@ def test_position_discrimination_sharpened_scores():
     """Sharpened scores (queries scaled by 8, nearly one-hot softmax).  Two things change against the unsharpened
     case, both visible in the CPU emulation of the kernels' bf16 rounding points (tests/bf16_emulation.py):
      - the bf16 rounding of the rotated keys is amplified 8x in the scores, so the error against the fp64 oracle
-       exceeds the spec bar (emulated max / mean 3.9e-2..5.3e-2 / 2.7e-3..3.1e-3 on seeds 71-73 of this
+       exceeds the spec bar (emulated max / mean 3.9e-2..6.6e-2 / 2.7e-3..3.3e-3 on seeds 71-74 of this
        recipe; the GPU's own max error is held to 1.5x the emulated one, computed here);
      - a chunk whose keys carry no mass moves the output very little when shifted, so against the fp64 oracle
        the shift margin falls to 1.2x-1.9x (mean error).
     Discrimination is therefore checked against the emulation itself, which rounds where the kernels round: for
-    every chunk and shift +-1 the GPU result must be at least 3x closer (mean error over the request's rows) to the
-    emulation at the true positions than to the emulation with that chunk shifted.  On this workload (seed 74) the
-    smallest emulated displacement of a shift is 4.0e-3 (mean) against 3.8e-3 mean error of the emulation itself
-    against the oracle."""
+    every chunk and shift +-1 the GPU result must be at least 10x closer (mean error over the request's rows) to
+    the emulation at the true positions than to the emulation with that chunk shifted.  On this workload (seed 74)
+    the smallest emulated displacement of a shift is 4.0e-3 (mean), the emulation's own error against the oracle
+    is 6.6e-2 / 3.3e-3 (max / mean), and on an MI355X the kernels' output lies 9.3e-5 (mean) from the emulation,
+    a worst shift margin of 42x."""
     import bf16_emulation as E
 
     w = W.custom(74, 4, 2, 128, 1e4, DISCRIMINATION_REQS)
@@ -325,7 +326,7 @@ def test_position_discrimination_sharpened_scores():
             w2.chunks["pos_offset"][i] += d
             d1 = np.abs(o[rows] - E.emulate(w2)[rows]).mean()
             worst = min(worst, d1 / max(d0, 1e-12))
-            assert d1 > 3 * d0, (i, d, d0, d1)
+            assert d1 > 10 * d0, (i, d, d0, d1)
     print(f"sharpened: worst shift margin against the emulation {worst:.1f}x", flush=True)
 
 
