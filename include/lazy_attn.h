@@ -166,6 +166,30 @@ LAZY_API int lazy_attn_decode(const lazy_attn_params_t* params, const void* q, c
 LAZY_API size_t lazy_attn_decode_workspace_size(const lazy_attn_params_t* params, int32_t batch, int32_t max_kv_len);
 
 /*
+ * Decode that allocates nothing and takes no workspace, for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation).  Same arguments, kernels and results
+ * as lazy_attn_decode; the split-KV partial results go to a fixed device array of LAZY_NOALLOC_SCRATCH_BYTES inside
+ * the library instead of a caller workspace (each device the library runs on holds its own copy until the process
+ * ends).
+ *  - The first call on a device looks up that device's copy (hipGetSymbolAddress, which may make the HIP runtime
+ *    load the library's code object on that device); later calls only launch.  The library itself calls no
+ *    allocating routine.
+ *  - `stream` (NULL = the null stream) must belong to the calling thread's current device: LAZY_EINVAL otherwise.
+ *  - LAZY_EWORKSPACE if the launch needs more than LAZY_NOALLOC_SCRATCH_BYTES, i.e. if
+ *    lazy_attn_decode_workspace_size(params, batch, max_kv_len) exceeds it; nothing is launched then.  Every launch
+ *    with the library's own split count (params->num_splits = 0) fits: it needs less than
+ *    1024 * min(G, 16) * (2 D + 4) bytes (4.3 MB at D = 128).
+ *  - Every call on one device shares the array, which keeps the last call's contents.  Each launch writes every
+ *    partial result it later reads, so nothing needs clearing between calls, but calls that overlap on one device
+ *    (on different streams, or from different host threads without ordering) race on it and give wrong results.
+ */
+#define LAZY_NOALLOC_SCRATCH_BYTES (8 << 20)
+LAZY_API int lazy_attn_decode_noalloc(const lazy_attn_params_t* params, const void* q, const int32_t* q_pos,
+                                      const void* k_pool, const void* v_pool, const lazy_chunk_t* chunks,
+                                      const int32_t* chunk_start, int32_t batch, int32_t max_kv_len, void* out,
+                                      float* lse, void* stream);
+
+/*
  * Split-KV merge (standard log-sum-exp combination of partial softmax results over disjoint key sets): each split s
  * holds its own normalised output o[s][row] and the log-sum-exp lse[s][row] of its scaled scores (natural log);
  * with M = max_s lse[s][row] and w_s = exp(lse[s][row] - M):

@@ -252,6 +252,29 @@ int lazy_plain_attn_decode(const lazy_attn_params_t* params, const void* q, cons
                     workspace, workspace_bytes, stream);
 }
 
+int lazy_attn_decode_noalloc(const lazy_attn_params_t* params, const void* q, const int32_t* q_pos,
+                             const void* k_pool, const void* v_pool, const lazy_chunk_t* chunks,
+                             const int32_t* chunk_start, int32_t batch, int32_t max_kv_len, void* out, float* lse,
+                             void* stream) {
+  const int e = check_params(params);
+  if (e != LAZY_OK) return e;
+  if (batch < 0 || max_kv_len < 0) return LAZY_EINVAL;
+  if (batch == 0) return LAZY_OK;
+  const size_t need = lazy_attn_decode_workspace_size(params, batch, max_kv_len);
+  if (need > (size_t)LAZY_NOALLOC_SCRATCH_BYTES) return LAZY_EWORKSPACE;
+  int device = -1;
+  if (hipGetDevice(&device) != hipSuccess) return LAZY_EHIP;
+  if (stream) {
+    hipDevice_t sd = -1;
+    if (hipStreamGetDevice(static_cast<hipStream_t>(stream), &sd) != hipSuccess) return LAZY_EHIP;
+    if (sd != device) return LAZY_EINVAL;
+  }
+  void* ws = nullptr;
+  if (lazy::noalloc_scratch(device, &ws) != hipSuccess) return LAZY_EHIP;
+  return run_decode(true, params, q, q_pos, k_pool, v_pool, chunks, chunk_start, batch, max_kv_len, out, lse, ws,
+                    (size_t)LAZY_NOALLOC_SCRATCH_BYTES, stream);
+}
+
 int lazy_attn_combine(const void* part_o, const float* part_lse, int32_t splits, int32_t rows, int32_t head_dim,
                       void* out, float* lse, void* stream) {
   if (head_dim != 64 && head_dim != 128) return LAZY_EUNSUPPORTED;

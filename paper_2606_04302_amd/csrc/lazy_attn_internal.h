@@ -76,6 +76,9 @@ hipError_t launch_prefill(const AttnArgs& a, int head_dim, bool rotate_k, hipStr
 hipError_t launch_decode(const AttnArgs& a, int head_dim, bool rotate_k, hipStream_t stream);
 hipError_t launch_decode_shared(const SharedArgs& a, int num_items, int max_slots, const int32_t* slot_start,
                                 int head_dim, uint16_t* out, float* lse, hipStream_t stream);
+// Device address of the fixed scratch array of lazy_attn_decode_noalloc on `device`, which must be the calling
+// thread's current device; looked up once per device and cached.
+hipError_t noalloc_scratch(int device, void** ptr);
 hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int splits, int rows, int head_dim,
                           uint16_t* out, float* lse, hipStream_t stream);
 hipError_t launch_materialize(const uint16_t* k_pool, const lazy_chunk_t* chunks, int num_records,

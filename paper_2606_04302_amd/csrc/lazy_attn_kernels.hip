@@ -36,6 +36,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "lazy_attn_internal.h"
 
 namespace lazy {
@@ -1867,6 +1869,29 @@ hipError_t combine_dispatch(const uint16_t* part_o, const float* part_lse, int s
 }
 
 }  // namespace
+
+// Split-KV partial results of lazy_attn_decode_noalloc: a fixed device array that every call on a device shares,
+// for callers that cannot allocate.  Each device holds its own copy for the life of the process.  Host code never
+// uses this name as an address: its device address comes from hipGetSymbolAddress (noalloc_scratch below).
+static __device__ __align__(256) unsigned char scratch[LAZY_NOALLOC_SCRATCH_BYTES];
+
+hipError_t noalloc_scratch(int device, void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* per_device[kMaxDevices] = {};
+  *ptr = nullptr;
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!per_device[device]) {
+    // The calling thread's current device is `device` (checked by the caller): the address is that device's copy.
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    per_device[device] = p;
+  }
+  *ptr = per_device[device];
+  return hipSuccess;
+}
 
 hipError_t launch_combine(const uint16_t* part_o, const float* part_lse, int splits, int rows, int head_dim,
                           uint16_t* out, float* lse, hipStream_t st) {

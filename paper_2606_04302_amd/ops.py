@@ -66,6 +66,8 @@ SIGNATURES = {
     "lazy_attn_decode": (_c_i32, _ATTN_DECODE),
     "lazy_plain_attn_decode": (_c_i32, _ATTN_DECODE),
     "lazy_attn_decode_workspace_size": (_c_sz, [ctypes.POINTER(LazyAttnParams), _c_i32, _c_i32]),
+    "lazy_attn_decode_noalloc": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32,
+                                          _c_i32, _c_p, _c_p, _c_p]),
     "lazy_attn_combine": (_c_i32, [_c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p]),
     "lazy_materialize_k": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_i32, _c_i32, _c_i64, _c_p, _c_p,
                                     _c_p]),
@@ -252,6 +254,35 @@ def decode(cfg: Config, q, q_pos, k_pool, v_pool, chunks, chunk_start, max_kv_le
               chunks.data_ptr(), chunk_start.data_ptr(), batch, max_kv_len, out.data_ptr(), _ptr(lse),
               _ptr(workspace), nbytes, _stream(stream)),
            "lazy_plain_attn_decode" if plain else "lazy_attn_decode")
+    return out, lse
+
+
+NOALLOC_SCRATCH_BYTES = 8 << 20  # LAZY_NOALLOC_SCRATCH_BYTES
+
+
+def decode_noalloc(cfg: Config, q, q_pos, k_pool, v_pool, chunks, chunk_start, max_kv_len: int, out, lse=None,
+                   stream=None):
+    """lazy_attn_decode_noalloc: lazy_attn_decode with the split partials in the library's fixed device array.
+    The caller passes the output (nothing is allocated here either).  Returns (out, lse)."""
+    _dev(q, torch.bfloat16, "q")
+    _dev(k_pool, torch.bfloat16, "k_pool")
+    _dev(v_pool, torch.bfloat16, "v_pool")
+    _dev(q_pos, torch.int32, "q_pos")
+    _dev(chunk_start, torch.int32, "chunk_start")
+    _chunks(chunks)
+    _need(q.dim() == 3 and q.shape[1] == cfg.num_q_heads and q.shape[2] == cfg.head_dim, "q must be [B, Hq, D]")
+    batch = q.shape[0]
+    _need(chunk_start.numel() == batch + 1 and q_pos.numel() == batch, "table sizes disagree with the batch")
+    _dev(out, torch.bfloat16, "out")
+    _need(out.shape == q.shape, "out must have the shape of q")
+    if lse is not None:
+        _dev(lse, torch.float32, "lse")
+        _need(lse.shape == (batch, cfg.num_q_heads), "lse must be [B, Hq]")
+    p = cfg.c()
+    _check(lib().lazy_attn_decode_noalloc(ctypes.byref(p), q.data_ptr(), q_pos.data_ptr(), k_pool.data_ptr(),
+                                          v_pool.data_ptr(), chunks.data_ptr(), chunk_start.data_ptr(), batch,
+                                          max_kv_len, out.data_ptr(), _ptr(lse), _stream(stream)),
+           "lazy_attn_decode_noalloc")
     return out, lse
 
 

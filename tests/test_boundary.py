@@ -168,6 +168,20 @@ def test_scalar_argument_errors_return_before_any_launch(ops):
                               None) == ops.LAZY_EINVAL
     assert L.lazy_attn_decode(ctypes.byref(good), fake, fake, fake, fake, fake, fake, 0, 100, fake, None, None, 0,
                               None) == ops.LAZY_OK
+    # decode without allocation: argument checks and the scratch limit come before any HIP call
+    noalloc = lambda p, batch=2, max_kv=100: L.lazy_attn_decode_noalloc(
+        ctypes.byref(p) if p is not None else None, fake, fake, fake, fake, fake, fake, batch, max_kv, fake, None, None)
+    assert noalloc(None) == ops.LAZY_EINVAL
+    assert noalloc(P(8, 2, 96, 1, 1e4, 0.0, None, 0, 0)) == ops.LAZY_EUNSUPPORTED
+    assert noalloc(good, batch=-1) == ops.LAZY_EINVAL
+    assert noalloc(good, batch=0) == ops.LAZY_OK
+    many = P(32, 8, 128, 1, 5e5, 0.0, None, 64, 0)  # 64 splits x 64 x 32 rows x 260 B = 34 MB of partials
+    assert noalloc(many, batch=64, max_kv=1 << 20) == ops.LAZY_EWORKSPACE
+    # the default split count always fits the scratch array (about 1024 * min(G, 16) rows at most)
+    for hq, hkv, d in ((32, 8, 128), (64, 4, 128), (16, 16, 64), (128, 4, 128)):
+        cfg = ops.Config(hq, hkv, d, 1e4)
+        for batch in (1, 2, 3, 5, 31, 64, 200):
+            assert ops.decode_workspace_size(cfg, batch, 1 << 20) <= ops.NOALLOC_SCRATCH_BYTES, (hq, hkv, d, batch)
     # combine / materialize
     assert L.lazy_attn_combine(fake, fake, 0, 10, 128, fake, None, None) == ops.LAZY_EINVAL
     assert L.lazy_attn_combine(fake, fake, 2, 10, 80, fake, None, None) == ops.LAZY_EUNSUPPORTED

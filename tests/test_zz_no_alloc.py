@@ -1,0 +1,66 @@
+"""lazy_attn_decode_noalloc (split-KV partials in the library's fixed device array, for callers that cannot
+allocate) against lazy_attn_decode (caller workspace): the same kernels, so the same bits, on consecutive calls that
+share the array, the later ones smaller; and both within the benchmark spec's tolerance of the fp64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import lazy_oracle as O
+from paper_2606_04302_amd import ops
+from paper_2606_04302_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ops.lib()
+    yield
+
+
+def _both(w, ckw):
+    dw = ops.upload(w)
+    cfg = ops.config_of(w, **ckw)
+    ref_out, ref_lse = ops.run_lazy(dw, cfg)  # lazy_attn_decode with a workspace from torch
+    out = torch.full_like(dw.q, float("nan"))
+    lse = torch.full_like(ref_lse, float("nan"))
+    ops.decode_noalloc(cfg, dw.q, dw.q_pos0, dw.pool, dw.pool, dw.chunks, dw.chunk_start, max(1, w.max_kv_len), out,
+                       lse)
+    torch.cuda.synchronize()
+    return out, lse, ref_out, ref_lse
+
+
+def test_noalloc_decode_matches_decode_on_consecutive_calls():
+    w1 = W.rag_decode(seed=171, batch=6, hq=8, hkv=2, d=128, n_chunks=5, chunk_len=200, pool_chunks=7, tail_len=9,
+                      tail_cap=16)
+    w2 = W.rag_decode(seed=172, batch=3, hq=8, hkv=2, d=128, n_chunks=3, chunk_len=120, pool_chunks=4, tail_len=3,
+                      tail_cap=8)
+    w3 = W.icl_decode_step(W.icl_prefill(seed=3), 5)  # full size: 4 x 33K keys, the default 16 splits (0.53 MB)
+    cases = [(w1, dict(num_splits=7), "6 requests, 7 splits"), (w2, dict(num_splits=3), "3 requests, 3 splits"),
+             (w2, {}, "3 requests, default splits"), (w3, {}, "icl decode step, default splits"),
+             (w1, dict(num_splits=5), "6 requests, 5 splits, after the larger call")]
+    for w, ckw, tag in cases:
+        need = ops.decode_workspace_size(ops.config_of(w, **ckw), w.batch, max(1, w.max_kv_len))
+        assert need <= ops.NOALLOC_SCRATCH_BYTES
+        print(f"noalloc {tag}: {need} bytes of partials", flush=True)
+        out, lse, ref_out, ref_lse = _both(w, ckw)
+        assert torch.equal(out.view(torch.int16), ref_out.view(torch.int16)), tag
+        assert torch.equal(lse, ref_lse), tag
+        ref_o, ref_l = O.lazy_decode(w.q, w.q_pos0, w.pool, w.pool, w.chunks, w.chunk_start, w.num_q_heads,
+                                     w.num_kv_heads, w.head_dim, w.rope_base, w.causal)
+        err = np.abs(out.float().cpu().numpy() - ref_o)
+        assert err.max() <= 2e-2 and err.mean() <= 2e-3, (tag, err.max(), err.mean())
+        assert np.abs(lse.cpu().numpy() - ref_l).max() <= 2e-2, tag
+
+
+def test_noalloc_decode_rejects_partials_beyond_the_array():
+    w = W.rag_decode(seed=173, batch=64, hq=32, hkv=8, d=128, n_chunks=2, chunk_len=64, pool_chunks=3, tail_len=2,
+                     tail_cap=4)
+    dw = ops.upload(w)
+    cfg = ops.config_of(w, num_splits=64)  # 64 x 2048 rows x 260 B = 34 MB > 8 MiB: refused before any launch
+    out = torch.empty_like(dw.q)
+    with pytest.raises(ops.LazyAttnError) as e:
+        ops.decode_noalloc(cfg, dw.q, dw.q_pos0, dw.pool, dw.pool, dw.chunks, dw.chunk_start, w.max_kv_len, out)
+    assert "workspace" in str(e.value)
