@@ -68,6 +68,49 @@ def timed(fn, steps: int, warmup: int):
     return start.elapsed_time(end) / steps
 
 
+def clock_warmup(fn, min_ms: float = 150.0):
+    """Back-to-back calls of ``fn`` until at least ``min_ms`` of GPU time has elapsed (HIP events), so that the
+    clocks have left their idle state before anything is timed; returns the GPU ms spent.  Independent of the
+    --warmup step count, which is still honoured as given before every timed leg."""
+    import torch
+
+    spent, batch = 0.0, 8
+    while spent < min_ms:
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(batch):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        spent += a.elapsed_time(b)
+        batch = min(batch * 2, 4096)
+    return spent
+
+
+def paired_overhead(fn, base, loops: int = 15, inner: int = 20):
+    """Relative cost of ``fn`` over ``base``: ``loops`` pairs of timed loops of ``inner`` back-to-back calls each,
+    the two alternating so that clock drift affects both alike; the median, smallest and largest of the per-pair
+    ratios minus one."""
+    import torch
+
+    ratios = []
+    for _ in range(loops):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record()
+        for _ in range(inner):
+            fn()
+        ev[1].record()
+        ev[2].record()
+        for _ in range(inner):
+            base()
+        ev[3].record()
+        torch.cuda.synchronize()
+        ratios.append(ev[0].elapsed_time(ev[1]) / ev[2].elapsed_time(ev[3]) - 1.0)
+    return {"median": round(float(np.median(ratios)), 4), "min": round(float(min(ratios)), 4),
+            "max": round(float(max(ratios)), 4), "pairs": loops, "calls_per_loop": inner}
+
+
 def timed_graph(fn, reps: int, inner: int = 20):
     """Average ms per call of a short GPU call whose host-side launch cost would otherwise dominate: ``inner``
     calls captured in one HIP graph, the graph replayed ``reps`` times between HIP events."""
@@ -321,6 +364,8 @@ def other_configs(dev, steps: int, warmup: int, log):
     ms = timed(e3(cfg), steps, warmup)
     norot = timed(e3(cfg, True), steps, warmup)
     local = timed(e3(ops.config_of(w, key_positions=ops.KEYS_LOCAL)), steps, warmup)
+    e3_spread = paired_overhead(e3(cfg), e3(cfg, True))
+    e3_local_spread = paired_overhead(e3(ops.config_of(w, key_positions=ops.KEYS_LOCAL)), e3(cfg, True))
     mat_fn, k_mat, ch_mat = materialized(w, dw, w.chunks)
     mat_ms = timed(mat_fn, max(5, steps // 5), 2)
     res["e3_overhead"] = {
@@ -330,8 +375,10 @@ def other_configs(dev, steps: int, warmup: int, log):
         "tflops": round(flops / (ms * 1e-3) / 1e12, 3),
         "no_rotation_ms": round(norot, 5),
         "rotation_overhead": round(ms / norot - 1.0, 4),
+        "rotation_overhead_spread": e3_spread,
         "local_keys_ms": round(local, 5),
         "local_keys_overhead": round(local / norot - 1.0, 4),
+        "local_keys_overhead_spread": e3_local_spread,
         "materialize_ms": round(mat_ms, 5),
         "speedup_vs_materialize": round((mat_ms + norot) / ms, 3),
     }
@@ -416,7 +463,8 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=500,
-                    help="untimed steps first; the GPU clocks need some tens of ms of load to settle")
+                    help="untimed steps before every timed leg (a time-based clock warm-up of >= 150 ms of GPU "
+                         "work runs once before the first leg whatever this is)")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode and baseline legs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-other", action="store_true", help="skip the ICL and variable-length RAG configurations")
@@ -460,6 +508,8 @@ def main() -> int:
                     wp.max_kv_len, out=out, lse=lse, workspace=ws)
 
     torch.cuda.synchronize()
+    log("prefill: clock warm-up")
+    warm_ms = clock_warmup(prefill)
     log(f"prefill: timing {args.steps} steps after {args.warmup} warmup")
     ms = timed(prefill, args.steps, args.warmup)
 
@@ -481,9 +531,10 @@ def main() -> int:
     cold_ms = timed_cold(prefill, max(10, args.steps // 10))
 
     # No-rotation diagnostic: the same kernel with K rotation compiled out, over the unrotated store.
-    norot_ms = timed(lambda: ops.prefill(cfg, dp.q, dp.q_start, dp.q_pos0, dp.pool, dp.pool, dp.chunks,
-                                         dp.chunk_start, wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws,
-                                         plain=True), args.steps, args.warmup)
+    norot = lambda: ops.prefill(cfg, dp.q, dp.q_start, dp.q_pos0, dp.pool, dp.pool, dp.chunks, dp.chunk_start,
+                                wp.max_q_len, wp.max_kv_len, out=out, lse=lse, workspace=ws, plain=True)
+    norot_ms = timed(norot, args.steps, args.warmup)
+    rot_spread = paired_overhead(prefill, norot)
 
     # The same batch over a local-position key store (keys kept encoded at their local index; one rotation per
     # record offset).  The pool's values are read as such keys: same shapes and traffic.
@@ -532,6 +583,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
+        "clock_warmup_ms": round(warm_ms, 1),
         "config": {
             "workload": "rag_prefill: Llama-3-8B-shaped RAG prefill, batch 8, 32 query / 8 KV heads, head_dim 128, "
                         "RoPE base 5e5, 128-token shared prefix + 10 x 512-token chunks drawn from a 64-chunk pool "
@@ -565,6 +617,7 @@ def main() -> int:
             "cold_cache_tflops": round(flops / (cold_ms * 1e-3) / 1e12, 3),
             "no_rotation_ms": round(norot_ms, 5),
             "rotation_overhead": round(ms / norot_ms - 1.0, 4),
+            "rotation_overhead_spread": rot_spread,
             "local_keys_ms": round(local_ms, 5),
             "local_keys_tflops": round(flops / (local_ms * 1e-3) / 1e12, 3),
             "paged64_ms": round(paged_ms, 5),
@@ -596,9 +649,12 @@ def main() -> int:
         dcold = timed_cold(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
                                               wd.max_kv_len, out=outd, lse=lsed, workspace=wsd),
                            max(10, args.steps // 20))
-        dnorot = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
-                                          wd.max_kv_len, out=outd, lse=lsed, workspace=wsd, plain=True),
-                       args.steps, args.warmup)
+        dec_lazy = lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
+                                      wd.max_kv_len, out=outd, lse=lsed, workspace=wsd)
+        dec_norot = lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
+                                       wd.max_kv_len, out=outd, lse=lsed, workspace=wsd, plain=True)
+        dnorot = timed(dec_norot, args.steps, args.warmup)
+        drot_spread = paired_overhead(dec_lazy, dec_norot)
         cfgd_local = ops.config_of(wd, key_positions=ops.KEYS_LOCAL)
         dlocal = timed(lambda: ops.decode(cfgd_local, dd.q, dd.q_pos0, dd.pool, dd.pool, dd.chunks, dd.chunk_start,
                                           wd.max_kv_len, out=outd, lse=lsed, workspace=wsd), args.steps, args.warmup)
@@ -652,6 +708,7 @@ def main() -> int:
             "splits": int(wsd_bytes // (wd.batch * wd.num_q_heads * (2 * wd.head_dim + 4))) if wsd_bytes else 1,
             "no_rotation_ms": round(dnorot, 5),
             "rotation_overhead": round(dms / dnorot - 1.0, 4),
+            "rotation_overhead_spread": drot_spread,
             "local_keys_ms": round(dlocal, 5),
             "local_keys_logical_hbm_gbps": round(dbytes / (dlocal * 1e-3) / 1e9, 1),
             "shared_ms": round(dshared, 5),
