@@ -1619,9 +1619,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 // ---------------------------------------------------------------------------------------------------------------
 // Split-KV merge: per row, the splits' normalised outputs weighted by exp(lse_s - max lse), divided by the sum of
 // the weights.  A row is served by CG x D / 8 lanes of one wave: lane (g, d8) loads 8 dims (16 bytes) of the
-// splits g, g + CG, ... (several at once); with CG > 1 the groups' partial sums are then added across lanes.
-// Every thread first reads all of the row's log-sum-exps (independent loads, one round trip), so a merge costs
-// two memory round trips rather than one per split.  CG = 1 for a few splits, 4 for many.
+// splits g, g + CG, ... together with their log-sum-exps, U splits per memory round trip, and keeps a running
+// maximum, weight sum and weighted sum (rescaled when the maximum grows); with CG > 1 the groups' states are then
+// merged across lanes.  A merge of up to U x CG splits thus costs one memory round trip.  CG = 1 for a few splits,
+// 4 for many.
 // ---------------------------------------------------------------------------------------------------------------
 template <int D, int CG>
 __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __restrict__ part_o,
@@ -1630,7 +1631,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __res
                                                            uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int TPR = D / 8;
   constexpr int LPR = TPR * CG;        // lanes per row
-  constexpr int U = 4;                 // splits loaded together per lane: up to 4 CG splits per round trip
+  constexpr int U = 4;                 // splits loaded together per lane
   static_assert(LPR <= 64 && 64 % LPR == 0, "a row's lanes lie in one wave");
   const int row = blockIdx.x * (kThreads / LPR) + threadIdx.x / LPR;
   const int d8 = threadIdx.x % TPR;
@@ -1639,18 +1640,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __res
   const bool live = row < rows;
   // With slot_start (shared decode), row r * hq + h of request r merges that request's own slot count.
   if (live && slot_start) splits = slot_start[row / hq + 1] - slot_start[row / hq];
-  float mmax = -INFINITY;
+  float m = -INFINITY, den = 0.f, sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (live) {
-    for (int s0 = 0; s0 < splits; s0 += 16) {  // 16 log-sum-exps per round trip
-      float l[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e) l[e] = s0 + e < splits ? part_lse[(int64_t)(s0 + e) * rows + row] : -INFINITY;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mmax = fmaxf(mmax, l[e]);
-    }
-  }
-  float den = 0.f, sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  if (live && mmax != -INFINITY) {
     for (int s0 = grp; s0 < splits; s0 += U * CG) {
       float ls[U];
       u32x4 v[U];
@@ -1661,10 +1652,21 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __res
         ls[e] = sp < splits ? part_lse[w] : -INFINITY;
         v[e] = *reinterpret_cast<const u32x4*>(part_o + w * D + 8 * d8);
       }
+      float mb = ls[0];
+#pragma unroll
+      for (int e = 1; e < U; ++e) mb = fmaxf(mb, ls[e]);
+      if (mb == -INFINITY) continue;  // every split here is empty
+      if (mb > m) {
+        const float c = expf(m - mb);  // 0 while nothing has been added (m = -inf)
+        den *= c;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) sum[k] *= c;
+        m = mb;
+      }
 #pragma unroll
       for (int e = 0; e < U; ++e) {
         if (ls[e] == -INFINITY) continue;  // an empty split contributes nothing, whatever its output holds
-        const float sc = expf(ls[e] - mmax);
+        const float sc = expf(ls[e] - m);
         den += sc;
 #pragma unroll
         for (int k = 0; k < 8; ++k) sum[k] = fmaf((k & 1) ? bf_hi(v[e][k >> 1]) : bf_lo(v[e][k >> 1]), sc, sum[k]);
@@ -1673,16 +1675,20 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __res
   }
 #pragma unroll
   for (int off = TPR; off < LPR; off *= 2) {
-    den += __shfl_xor(den, off);
+    const float mo = __shfl_xor(m, off);
+    const float mn = fmaxf(m, mo);
+    const float c0 = m == -INFINITY ? 0.f : expf(m - mn), c1 = mo == -INFINITY ? 0.f : expf(mo - mn);
+    den = den * c0 + __shfl_xor(den, off) * c1;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) sum[k] += __shfl_xor(sum[k], off);
+    for (int k = 0; k < 8; ++k) sum[k] = sum[k] * c0 + __shfl_xor(sum[k], off) * c1;
+    m = mn;
   }
   if (!live || grp != 0) return;
   const float inv = den > 0.f ? 1.f / den : 0.f;
   *reinterpret_cast<u32x4*>(out + (int64_t)row * D + 8 * d8) =
       u32x4{pack2(sum[0] * inv, sum[1] * inv), pack2(sum[2] * inv, sum[3] * inv), pack2(sum[4] * inv, sum[5] * inv),
             pack2(sum[6] * inv, sum[7] * inv)};
-  if (lse && d8 == 0) lse[row] = den > 0.f ? mmax + logf(den) : -INFINITY;
+  if (lse && d8 == 0) lse[row] = den > 0.f ? m + logf(den) : -INFINITY;
 }
 
 // ---------------------------------------------------------------------------------------------------------------
@@ -1879,7 +1885,7 @@ hipError_t combine_d(const uint16_t* part_o, const float* part_lse, int splits, 
 hipError_t combine_dispatch(const uint16_t* part_o, const float* part_lse, int splits, int rows,
                             const int32_t* slot_start, int hq, int head_dim, uint16_t* out, float* lse,
                             hipStream_t st) {
-  const bool few = splits <= 8;
+  const bool few = splits <= 4;  // one round trip with one lane group per row
   if (head_dim == 128)
     return few ? combine_d<128, 1>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st)
                : combine_d<128, 4>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
