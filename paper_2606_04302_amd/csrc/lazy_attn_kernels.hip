@@ -875,6 +875,13 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
   ld.load_constants(sm.csd);
 
   // Tile "ahead" state for NBUF == 2: position of the tile after the current one.
+  // Eight-wave workgroups: waves w and w + 4 share a SIMD, and the tile barrier would keep them in the same phase
+  // (both feeding the matrix core, then both on the vector ALU).  The upper four waves therefore store their share
+  // of the next tile at the start of the interval and fetch theirs one tile further ahead, while the lower four
+  // store theirs at the end: the two waves on a SIMD alternate between MFMA and VALU phases.  Both halves of a tile
+  // are in LDS by the barrier that ends the interval before it is read; the buffer they overwrite was last read in
+  // the interval before (double buffering is enough).
+  const bool early = NBUF == 2 && NW == 8 && uniform(wave) >= NW / 2;
   TileIter<kSub> ahead = it;
   bool have_ahead = false;
   if (have && NBUF == 2) {
@@ -885,6 +892,9 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
       prefill_base<D, LOCAL>(sm.csb[1][0], sm.freq, tid, ahead.cur.pos + (LOCAL ? 0 : ahead.j0));
     __syncthreads();
     ld.store(sm.k[0], sm.v[0], sm.csb[0][0], sm.csd);
+    if (early && have_ahead)
+      ld.fetch(k_ptr(a.k_pool, ahead.cur, g, ahead.j0, D), v_ptr(a.v_pool, ahead.cur, g, ahead.j0, D),
+               min(kSub, ahead.cur.len - ahead.j0));
     __syncthreads();
   }
   int parity = 0;
@@ -907,11 +917,16 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
       cur_buf = parity;
       it = ahead;  // the next tile
       have_next = have_ahead;
+      if (early && have_next) ld.store(sm.k[parity ^ 1], sm.v[parity ^ 1], sm.csb[parity ^ 1][0], sm.csd);
       if (have_next) {
-        ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
-                 min(kSub, it.cur.len - it.j0));
+        if (!early)
+          ld.fetch(k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+                   min(kSub, it.cur.len - it.j0));
         ahead.step();
         have_ahead = ahead.seek(a.causal, qmax);
+        if (early && have_ahead)
+          ld.fetch(k_ptr(a.k_pool, ahead.cur, g, ahead.j0, D), v_ptr(a.v_pool, ahead.cur, g, ahead.j0, D),
+                   min(kSub, ahead.cur.len - ahead.j0));
       }
     }
     attend_tile<D, NT, RB, ALIBI>(sm.k[cur_buf], sm.v[cur_buf], lane, qf, o, m2, lsum, qpos, b0, nvalid, qmin,
@@ -920,7 +935,7 @@ __attribute__((amdgpu_waves_per_eu(RB == 1 ? 2 : 1, RB == 1 ? 2 : 1))) void pref
       // Base angles two tiles ahead go to the table slot this tile used; the next tile goes to the other buffer.
       if (ROT && have_ahead)
         prefill_base<D, LOCAL>(sm.csb[parity][0], sm.freq, tid, ahead.cur.pos + (LOCAL ? 0 : ahead.j0));
-      if (have_next) ld.store(sm.k[parity ^ 1], sm.v[parity ^ 1], sm.csb[parity ^ 1][0], sm.csd);
+      if (!early && have_next) ld.store(sm.k[parity ^ 1], sm.v[parity ^ 1], sm.csb[parity ^ 1][0], sm.csd);
       __syncthreads();
       parity ^= 1;
     }
