@@ -70,11 +70,11 @@ def timed(fn, steps: int, warmup: int):
 
 def clock_warmup(fn, min_ms: float = 150.0):
     """Back-to-back calls of ``fn`` until at least ``min_ms`` of GPU time has elapsed (HIP events), so that the
-    clocks have left their idle state before anything is timed; returns the GPU ms spent.  Independent of the
-    --warmup step count, which is still honoured as given before every timed leg."""
+    clocks have left their idle state before anything is timed; returns the GPU ms spent and the number of calls.
+    Independent of the --warmup step count, which is still honoured as given before every timed leg."""
     import torch
 
-    spent, batch = 0.0, 8
+    spent, batch, calls = 0.0, 8, 0
     while spent < min_ms:
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
@@ -84,8 +84,9 @@ def clock_warmup(fn, min_ms: float = 150.0):
         b.record()
         torch.cuda.synchronize()
         spent += a.elapsed_time(b)
+        calls += batch
         batch = min(batch * 2, 4096)
-    return spent
+    return spent, calls
 
 
 def paired_overhead(fn, base, loops: int = 15, inner: int = 20):
@@ -509,7 +510,7 @@ def main() -> int:
 
     torch.cuda.synchronize()
     log("prefill: clock warm-up")
-    warm_ms = clock_warmup(prefill)
+    warm_ms, warm_calls = clock_warmup(prefill)
     log(f"prefill: timing {args.steps} steps after {args.warmup} warmup")
     ms = timed(prefill, args.steps, args.warmup)
 
@@ -584,6 +585,7 @@ def main() -> int:
         "dtype": "bf16",
         "data": "synthetic",
         "clock_warmup_ms": round(warm_ms, 1),
+        "clock_warmup_calls": warm_calls,
         "config": {
             "workload": "rag_prefill: Llama-3-8B-shaped RAG prefill, batch 8, 32 query / 8 KV heads, head_dim 128, "
                         "RoPE base 5e5, 128-token shared prefix + 10 x 512-token chunks drawn from a 64-chunk pool "
