@@ -702,6 +702,28 @@ __device__ __forceinline__ void attend_tile(const uint16_t* kb, const uint16_t* 
       ps = ps0 + ps1;
     };
     float ps;
+    if constexpr (ALIBI) {
+      // ALiBi scores grow tile by tile towards the query, so the reference moves on most tiles: the maximum is
+      // taken first and the probabilities are formed once.
+      float mx = -INFINITY;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sa[rb][blk][i]);
+      mx = xor32_max(mx);
+      const float mt = mx * c;
+      if (__any(mt > m2[rb] + kRescaleSlack)) {
+        const float mnew = fmaxf(m2[rb], mt);
+        const float alpha = m2[rb] == -INFINITY ? 0.f : fast_exp2(m2[rb] - mnew);
+        lsum[rb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) o[rb][db] *= alpha;
+        m2[rb] = mnew;
+      }
+      form(m2[rb] == -INFINITY ? 0.f : m2[rb], ps);
+      lsum[rb] += ps;
+      continue;
+    }
     form(m2[rb] == -INFINITY ? 0.f : m2[rb], ps);
     if (__any(!(ps <= kRescaleBound) || m2[rb] == -INFINITY)) {
       float mx = -INFINITY;
