@@ -821,3 +821,22 @@ def test_positions_near_max_pos(mode):
                                              for r in reqs], kind="decode")
         run_and_check(wd, f"decode near 2^24 {mode} base {base:g}", ckw)
         run_shared_and_check(wd, f"shared decode near 2^24 {mode} base {base:g}", ckw)
+
+
+# --------------------------------------------------------------------------------------------------------------
+# The eight-wave prefill (256 packed rows: 64 tokens x G = 4) runs its upper four waves one tile ahead on the
+# loader side (they store their share of the next tile at the start of each interval).  Splits holding one, two or
+# three tiles start and end that pipeline in every way it can: no next tile, a next tile but none after it, and a
+# first tile that the causal rule skips (a record placed after the query ahead of visible ones).
+PHASE_REQS = [dict(chunks=[(64, 0)], q_len=64, q_pos0=64),
+              dict(chunks=[(10, 0), (64, 100), (40, 500)], q_len=64, q_pos0=600),
+              dict(chunks=[(64, 5000), (130, 0), (1, 300)], q_len=64, q_pos0=400)]
+
+
+@pytest.mark.parametrize("mode", ["nope", "local", "interleaved", "alibi"])
+def test_eight_wave_prefill_short_splits(mode):
+    ckw = OOO_MODES[mode]
+    w = W.custom(171, 8, 2, 128, 1e4, PHASE_REQS)
+    assert w.max_q_len * (w.num_q_heads // w.num_kv_heads) >= 256  # the eight-wave kernel
+    for splits in (1, 2, 3, 4, 6):
+        run_and_check(w, f"eight-wave prefill {mode} splits={splits}", {**ckw, "num_splits": splits})
