@@ -1658,17 +1658,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 // the weights.  A row is served by CG x D / 8 lanes of one wave: lane (g, d8) loads 8 dims (16 bytes) of the
 // splits g, g + CG, ... together with their log-sum-exps, U splits per memory round trip, and keeps a running
 // maximum, weight sum and weighted sum (rescaled when the maximum grows); with CG > 1 the groups' states are then
-// merged across lanes.  A merge of up to U x CG splits thus costs one memory round trip.  CG = 1 for a few splits,
-// 4 for many.
+// merged across lanes.  A merge of up to U x CG splits thus costs one memory round trip: CG = 1, U = 4 for up to 4
+// splits; CG = 4 with U = 8 (32 per round trip) up to 32, U = 16 (64 per round trip) beyond.
 // ---------------------------------------------------------------------------------------------------------------
-template <int D, int CG>
+template <int D, int CG, int U>
 __global__ __launch_bounds__(kThreads) void combine_kernel(const uint16_t* __restrict__ part_o,
                                                            const float* __restrict__ part_lse, int splits, int rows,
                                                            const int32_t* __restrict__ slot_start, int hq,
                                                            uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int TPR = D / 8;
   constexpr int LPR = TPR * CG;        // lanes per row
-  constexpr int U = 4;                 // splits loaded together per lane
   static_assert(LPR <= 64 && 64 % LPR == 0, "a row's lanes lie in one wave");
   const int row = blockIdx.x * (kThreads / LPR) + threadIdx.x / LPR;
   const int d8 = threadIdx.x % TPR;
@@ -1908,13 +1907,13 @@ void materialize_dk(bool local, bool il, dim3 grid, hipStream_t st, const uint16
   }
 }
 
-template <int D, int CG>
+template <int D, int CG, int U>
 hipError_t combine_d(const uint16_t* part_o, const float* part_lse, int splits, int rows, const int32_t* slot_start,
                      int hq, uint16_t* out, float* lse, hipStream_t st) {
   constexpr int per_block = kThreads / (D / 8 * CG);
   const dim3 grid((rows + per_block - 1) / per_block);
-  hipLaunchKernelGGL((combine_kernel<D, CG>), grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows, slot_start,
-                     hq, out, lse);
+  hipLaunchKernelGGL((combine_kernel<D, CG, U>), grid, dim3(kThreads), 0, st, part_o, part_lse, splits, rows,
+                     slot_start, hq, out, lse);
   return hipGetLastError();
 }
 
@@ -1922,12 +1921,14 @@ hipError_t combine_d(const uint16_t* part_o, const float* part_lse, int splits, 
 hipError_t combine_dispatch(const uint16_t* part_o, const float* part_lse, int splits, int rows,
                             const int32_t* slot_start, int hq, int head_dim, uint16_t* out, float* lse,
                             hipStream_t st) {
-  const bool few = splits <= 4;  // one round trip with one lane group per row
-  if (head_dim == 128)
-    return few ? combine_d<128, 1>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st)
-               : combine_d<128, 4>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
-  return few ? combine_d<64, 1>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st)
-             : combine_d<64, 4>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
+  if (head_dim == 128) {
+    if (splits <= 4) return combine_d<128, 1, 4>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
+    if (splits <= 32) return combine_d<128, 4, 8>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
+    return combine_d<128, 4, 16>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
+  }
+  if (splits <= 4) return combine_d<64, 1, 4>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
+  if (splits <= 32) return combine_d<64, 4, 8>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
+  return combine_d<64, 4, 16>(part_o, part_lse, splits, rows, slot_start, hq, out, lse, st);
 }
 
 }  // namespace

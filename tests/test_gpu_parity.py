@@ -205,7 +205,10 @@ def test_materialized_keys_match_oracle():
             base += 2 * n * 128
 
 
-@pytest.mark.parametrize("s,rows,d", [(5, 37, 128), (2, 300, 64), (13, 70, 128), (64, 9, 64)])
+# Split counts cover each merge variant (up to 4 splits; 5..32; more) and, past 64 splits, several rounds of loads
+# whose running maximum must be rescaled.
+@pytest.mark.parametrize("s,rows,d", [(5, 37, 128), (2, 300, 64), (3, 12, 128), (13, 70, 128), (32, 10, 128),
+                                      (33, 50, 128), (64, 9, 64), (129, 20, 128), (200, 11, 64)])
 def test_combine_entry_point_matches_oracle_merge(s, rows, d):
     rng = np.random.default_rng(5 + s)
     m = rng.normal(0, 3, size=(s, rows))
