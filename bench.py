@@ -286,6 +286,22 @@ def other_configs(dev, steps: int, warmup: int, log):
     log("icl: timing 128 decode steps")
     dec_ms = timed(decode_all, reps, 2)
 
+    # The same prefill and decode steps over a local-position store (keys kept encoded at their index within the
+    # chunk, the paper's own convention): the prefill rotates each K tile once by the record offset and the decode
+    # rotates the query once per record instead of every key.  Its materialising copy is the same one rotation per
+    # key as the NoPE store's, so it shares the baseline below.
+    cfg_local = ops.config_of(w, key_positions=ops.KEYS_LOCAL)
+    log("icl: timing the local-position store")
+    local_pre_ms = timed(lambda: ops.prefill(cfg_local, dw.q, dw.q_start, dw.q_pos0, dw.pool, dw.pool, dw.chunks,
+                                             dw.chunk_start, w.max_q_len, w.max_kv_len, out=out, workspace=ws),
+                         steps, warmup)
+
+    def decode_all_local():
+        for _, ch, qp in tables:
+            ops.decode(cfg_local, qd, qp, dw.pool, dw.pool, ch, dw.chunk_start, max_kv, out=outd, workspace=wsd)
+
+    local_dec_ms = timed(decode_all_local, reps, 2)
+
     # Chunk-major shared decode steps: the exemplar pool is read once per step for the four requests.
     plans = [ops.upload_plan(ops.shared_decode_plan(cfg, ch, w.chunk_start), dev) for ch, _, _ in tables]
     wsh = torch.empty(max(16, max(ops.decode_shared_workspace_size(cfg, w.batch, pl.max_slots) for pl in plans)),
@@ -344,6 +360,9 @@ def other_configs(dev, steps: int, warmup: int, log):
         "materialize_then_attend_ms": round(base_total, 4),
         "speedup_vs_materialize": round(base_total / lazy_total, 3),
         "speedup_vs_materialize_shared_decode": round(base_total / (pre_ms + shared_ms), 3),
+        "local_keys_prefill_ms": round(local_pre_ms, 5),
+        "local_keys_decode_128_steps_ms": round(local_dec_ms, 4),
+        "local_keys_speedup_vs_materialize": round(base_total / (local_pre_ms + local_dec_ms), 3),
     }
     del k_mat, dw, ws, wsd
 
