@@ -434,6 +434,13 @@ def other_configs(dev, steps: int, warmup: int, log):
 
     log("icl_private: timing 128 decode steps")
     pms = timed(decode_private, max(3, steps // 40), 2)
+    cfg_local = ops.config_of(w, key_positions=ops.KEYS_LOCAL)
+
+    def decode_private_local():  # the same steps over a local-position store (the query rotated once per record)
+        for ch, qp in tables:
+            ops.decode(cfg_local, qd, qp, dw.pool, dw.pool, ch, dw.chunk_start, max_kv, out=outd, workspace=wsd)
+
+    pms_local = timed(decode_private_local, max(3, steps // 40), 2)
     res["icl_private"] = {
         "workload": "icl with private pools: batch 4, 32/8 heads, head_dim 128, each request its own 128 x "
                     "256-token exemplars, 256-token query at 32,768, then 128 decode steps",
@@ -441,6 +448,8 @@ def other_configs(dev, steps: int, warmup: int, log):
         "decode_ms_per_step": round(pms / len(tables), 5),
         "decode_logical_hbm_gbps": round(pbytes / (pms * 1e-3) / 1e9, 1),
         "decode_logical_hbm_frac": round(pbytes / (pms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "local_keys_decode_128_steps_ms": round(pms_local, 4),
+        "local_keys_decode_logical_hbm_frac": round(pbytes / (pms_local * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
         "unique_kv_mb": round(A.unique_kv_bytes(w) / 1e6, 1),
     }
     del dw, wsd, tables
