@@ -51,10 +51,18 @@ def recorded_traffic(kernel: str):
     return entry.get("bytes_per_launch")
 
 
+LEG_WARMUP_MS = 30.0
+_last_leg_warmup_calls = 0
+
+
 def timed(fn, steps: int, warmup: int):
-    """Average ms per call, measured with HIP events on the current stream around ``steps`` back-to-back calls."""
+    """Average ms per call, measured with HIP events on the current stream around ``steps`` back-to-back calls.
+    Before them: at least LEG_WARMUP_MS of GPU time of the same call (so that every leg starts from its own working
+    set in the caches and from settled clocks, whatever the leg before it ran), then the --warmup calls."""
     import torch
 
+    global _last_leg_warmup_calls
+    _, _last_leg_warmup_calls = clock_warmup(fn, LEG_WARMUP_MS)
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
@@ -541,6 +549,7 @@ def main() -> int:
     warm_ms, warm_calls = clock_warmup(prefill)
     log(f"prefill: timing {args.steps} steps after {args.warmup} warmup")
     ms = timed(prefill, args.steps, args.warmup)
+    head_leg_calls = _last_leg_warmup_calls
 
     # The combine kernel alone on the same partials, to isolate the prefill kernel's own duration.
     rows = wp.total_q * wp.num_q_heads
@@ -614,6 +623,8 @@ def main() -> int:
         "data": "synthetic",
         "clock_warmup_ms": round(warm_ms, 1),
         "clock_warmup_calls": warm_calls,
+        "leg_warmup_ms": LEG_WARMUP_MS,
+        "headline_leg_warmup_calls": head_leg_calls,
         "config": {
             "workload": "rag_prefill: Llama-3-8B-shaped RAG prefill, batch 8, 32 query / 8 KV heads, head_dim 128, "
                         "RoPE base 5e5, 128-token shared prefix + 10 x 512-token chunks drawn from a 64-chunk pool "
