@@ -100,22 +100,28 @@ def clock_warmup(fn, min_ms: float = 150.0):
 def paired_overhead(fn, base, loops: int = 15, inner: int = 20):
     """Relative cost of ``fn`` over ``base``: ``loops`` pairs of timed loops of ``inner`` back-to-back calls each,
     the two alternating so that clock drift affects both alike; the median, smallest and largest of the per-pair
-    ratios minus one."""
+    ratios minus one.  Each pair starts with one untimed call, so that the GPU is already busy when the first event
+    is recorded (otherwise the first loop would also time the launch of its first call), and the pairs alternate
+    which of the two runs first."""
     import torch
 
     ratios = []
-    for _ in range(loops):
+    for i in range(loops):
+        first, second = (fn, base) if i % 2 == 0 else (base, fn)
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        first()
         ev[0].record()
         for _ in range(inner):
-            fn()
+            first()
         ev[1].record()
         ev[2].record()
         for _ in range(inner):
-            base()
+            second()
         ev[3].record()
         torch.cuda.synchronize()
-        ratios.append(ev[0].elapsed_time(ev[1]) / ev[2].elapsed_time(ev[3]) - 1.0)
+        t_first, t_second = ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+        t_fn, t_base = (t_first, t_second) if i % 2 == 0 else (t_second, t_first)
+        ratios.append(t_fn / t_base - 1.0)
     return {"median": round(float(np.median(ratios)), 4), "min": round(float(min(ratios)), 4),
             "max": round(float(max(ratios)), 4), "pairs": loops, "calls_per_loop": inner}
 
