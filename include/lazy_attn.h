@@ -83,6 +83,7 @@ typedef struct lazy_attn_params {
   int32_t key_positions; /* LAZY_KEYS_NOPE or LAZY_KEYS_LOCAL: how the chunk store holds its keys (below) */
   int32_t rope_style;    /* LAZY_ROPE_HALF, LAZY_ROPE_INTERLEAVED or LAZY_ALIBI: the positional method (below) */
   int32_t q_prerotated;  /* 0: q is position-free and the kernels rotate it; 1: q arrives already rotated (below) */
+  int32_t cache_hint;    /* LAZY_CACHE_DEFAULT or LAZY_CACHE_STREAM: how the decode reads K and V (below) */
 } lazy_attn_params_t;
 
 /*
@@ -108,6 +109,19 @@ typedef struct lazy_attn_params {
 #define LAZY_ROPE_HALF 0
 #define LAZY_ROPE_INTERLEAVED 1
 #define LAZY_ALIBI 2
+
+/*
+ * Cache hint for K and V (params->cache_hint; a performance choice only, results are bit-identical).
+ *  LAZY_CACHE_DEFAULT (0): ordinary loads.  Right whenever the call's chunks are shared between its requests, or are
+ *                          read again soon enough to still be in the last-level cache (a pool that fits in it).
+ *  LAZY_CACHE_STREAM  (1): the decode entry points (lazy_attn_decode, lazy_plain_attn_decode,
+ *                          lazy_attn_decode_noalloc) read K and V with non-temporal loads, which stream faster from
+ *                          HBM but give up the cache reuse above: for requests whose contexts are private and larger
+ *                          than the last-level cache, read once per decode step.  Other entry points ignore it.
+ * Any other value is LAZY_EINVAL.
+ */
+#define LAZY_CACHE_DEFAULT 0
+#define LAZY_CACHE_STREAM 1
 
 /*
  * Key-store conventions (params->key_positions).  Values and the causal rule are the same in both; only the

@@ -25,6 +25,7 @@ int check_params(const lazy_attn_params_t* p) {
     return LAZY_EINVAL;
   if (p->rope_style == LAZY_ALIBI && p->key_positions != LAZY_KEYS_NOPE) return LAZY_EINVAL;
   if (p->q_prerotated != 0 && p->q_prerotated != 1) return LAZY_EINVAL;
+  if (p->cache_hint != LAZY_CACHE_DEFAULT && p->cache_hint != LAZY_CACHE_STREAM) return LAZY_EINVAL;
   if (p->head_dim != 64 && p->head_dim != 128) return LAZY_EUNSUPPORTED;
   return LAZY_OK;
 }
@@ -198,6 +199,7 @@ int run_decode(bool rotate_k, const lazy_attn_params_t* p, const void* q, const 
   a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
   a.alibi = p->rope_style == LAZY_ALIBI;
   a.q_prerot = p->q_prerotated && p->rope_style != LAZY_ALIBI;
+  a.stream_kv = p->cache_hint == LAZY_CACHE_STREAM;
   return status(lazy::launch_decode(a, p->head_dim, rotate_k, static_cast<hipStream_t>(stream)));
 }
 

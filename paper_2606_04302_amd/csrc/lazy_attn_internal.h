@@ -37,6 +37,7 @@ struct AttnArgs {
   int32_t interleaved;        // 1: RoPE pairs (2t, 2t+1) (LAZY_ROPE_INTERLEAVED)
   int32_t alibi;              // 1: no rotation, ALiBi bias (LAZY_ALIBI); inv_freq then holds optional slopes
   int32_t q_prerot;           // 1: q arrives rotated at its own positions (rotations use -pos_offset / none)
+  int32_t stream_kv;          // decode: 1 reads K / V with non-temporal loads (LAZY_CACHE_STREAM)
   double rope_log2_base;      // log2(rope_base), computed on the host (unused with inv_freq)
   float scale_log2;           // softmax scale * log2(e)
 };

@@ -163,6 +163,9 @@ __device__ __forceinline__ float alibi_slope(int h, int hq, const float* table, 
 constexpr int kInterleaved = 4;
 constexpr int keys_of(int km) { return km & 3; }
 constexpr bool interleaved_of(int km) { return (km & kInterleaved) != 0; }
+// Bit 3 of a decode kernel's key-mode argument: K and V are read with non-temporal loads (LAZY_CACHE_STREAM).
+constexpr int kStreamKV = 8;
+constexpr bool stream_of(int km) { return (km & kStreamKV) != 0; }
 
 // 16 bf16 = pairs t0..t0+7 of an interleaved vector (w0: pairs t0..t0+3, one pair per 32-bit word, first element
 // in the low half; w1: pairs t0+4..t0+7) -> the first elements (lo) and second elements (hi) in pair order.
@@ -1074,15 +1077,20 @@ struct DecTile {
 // One key row's k-step pair s for this lane (pairs 32 s + 8 kq .. +7): first elements in lo, second in hi for
 // the half-split pairing; for the interleaved pairing the raw 16 elements (pairs_of splits them where they are
 // used, so that tiles in flight hold no extra registers).
-template <int D, bool IL>
+// A 16-byte load of K / V; NT: non-temporal (streamed from HBM without being kept for reuse).
+template <bool NT>
+__device__ __forceinline__ u32x4 kv_load(const uint16_t* p) {
+  if (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return *reinterpret_cast<const u32x4*>(p);
+}
+template <int D, bool IL, bool NT>
 __device__ __forceinline__ void dec_k_pairs(const uint16_t* krow, int s, int kq, u32x4& lo, u32x4& hi) {
   if (IL) {
-    const u32x4* src = reinterpret_cast<const u32x4*>(krow + 2 * (32 * s + 8 * kq));
-    lo = src[0];
-    hi = src[1];
+    lo = kv_load<NT>(krow + 2 * (32 * s + 8 * kq));
+    hi = kv_load<NT>(krow + 2 * (32 * s + 8 * kq) + 8);
   } else {
-    lo = *reinterpret_cast<const u32x4*>(krow + 32 * s + 8 * kq);
-    hi = *reinterpret_cast<const u32x4*>(krow + D / 2 + 32 * s + 8 * kq);
+    lo = kv_load<NT>(krow + 32 * s + 8 * kq);
+    hi = kv_load<NT>(krow + D / 2 + 32 * s + 8 * kq);
   }
 }
 
@@ -1096,7 +1104,7 @@ __device__ __forceinline__ void pairs_of(u32x4 a, u32x4 b, u32x4& lo, u32x4& hi)
   }
 }
 
-template <int D, bool IL>
+template <int D, bool IL, bool NT>
 __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, const uint16_t* vbase, int nvalid,
                                           int lane) {
   const int r = lane & 15, kq = lane >> 4;
@@ -1106,12 +1114,12 @@ __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, 
     for (int b = 0; b < 2; ++b) {
       const uint16_t* row = kbase + (size_t)kappa(b, r) * D;
 #pragma unroll
-      for (int s = 0; s < DecTile<D>::SP; ++s) dec_k_pairs<D, IL>(row, s, kq, t.k[b][s][0], t.k[b][s][1]);
+      for (int s = 0; s < DecTile<D>::SP; ++s) dec_k_pairs<D, IL, NT>(row, s, kq, t.k[b][s][0], t.k[b][s][1]);
     }
 #pragma unroll
     for (int i = 0; i < DecTile<D>::VC; ++i) {
       const int c = lane + 64 * i;
-      t.v[i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)(c / (D / 8)) * D + 8 * (c % (D / 8)));
+      t.v[i] = kv_load<NT>(vbase + (size_t)(c / (D / 8)) * D + 8 * (c % (D / 8)));
     }
     return;
   }
@@ -1123,7 +1131,7 @@ __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, 
 #pragma unroll
     for (int s = 0; s < DecTile<D>::SP; ++s) {
       u32x4 lo, hi;
-      dec_k_pairs<D, IL>(row, s, kq, lo, hi);
+      dec_k_pairs<D, IL, NT>(row, s, kq, lo, hi);
       t.k[b][s][0] = ok ? lo : zero;
       t.k[b][s][1] = ok ? hi : zero;
     }
@@ -1133,7 +1141,7 @@ __device__ __forceinline__ void dec_fetch(DecTile<D>& t, const uint16_t* kbase, 
     const int c = lane + 64 * i;
     const int key = c / (D / 8);
     const bool ok = key < nvalid;
-    const u32x4 x = *reinterpret_cast<const u32x4*>(vbase + (size_t)(ok ? key : 0) * D + 8 * (c % (D / 8)));
+    const u32x4 x = kv_load<NT>(vbase + (size_t)(ok ? key : 0) * D + 8 * (c % (D / 8)));
     t.v[i] = ok ? x : zero;
   }
 }
@@ -1252,7 +1260,7 @@ template <int D, int KMI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_kernel(AttnArgs a) {
   __shared__ DecodeSmem<D> sm;
   constexpr int KM = keys_of(KMI);
-  constexpr bool IL = interleaved_of(KMI), ALIBI = KM == kKeysAlibi;
+  constexpr bool IL = interleaved_of(KMI), ALIBI = KM == kKeysAlibi, NT = stream_of(KMI);
   // Keys are rotated in registers only for a NoPE store; with local-position keys the query is rotated by the
   // relative offset q_pos - pos_offset whenever the record changes (Sec. 3.2 "Decoding") and the keys are used as
   // stored.
@@ -1281,7 +1289,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   {
     const uint16_t* qrow = a.q + ((int64_t)r * a.hq + head) * D;
 #pragma unroll
-    for (int s = 0; s < SP; ++s) dec_k_pairs<D, IL>(qrow, s, kq, qraw[s][0], qraw[s][1]);
+    for (int s = 0; s < SP; ++s) dec_k_pairs<D, IL, false>(qrow, s, kq, qraw[s][0], qraw[s][1]);
   }
   if (!ALIBI && tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
   __syncthreads();
@@ -1299,7 +1307,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   bool have = it.seek_strided(a.causal, qpos, 4);
   DecTile<D> cur, nxt;
   if (have)
-    dec_fetch<D, IL>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+    dec_fetch<D, IL, NT>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
                  min(kDecWaveKeys, it.cur.len - it.j0), lane);
   if (ROT && have && lane < D / 2)
     *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
@@ -1394,7 +1402,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     it.skip(4);
     const bool have_next = it.seek_strided(a.causal, qpos, 4);
     if (have_next) {
-      dec_fetch<D, IL>(nxt, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
+      dec_fetch<D, IL, NT>(nxt, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
                    min(kDecWaveKeys, it.cur.len - it.j0), lane);
       if (ROT && lane < D / 2)
         *reinterpret_cast<float2*>(sm.csb[wave][buf ^ 1] + csb_idx<D>(lane)) =
@@ -1516,7 +1524,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
     for (int s = 0; s < SP; ++s) {
       qraw[s][0] = qraw[s][1] = u32x4{0, 0, 0, 0};
-      if (cvalid) dec_k_pairs<D, IL>(qrow, s, kq, qraw[s][0], qraw[s][1]);
+      if (cvalid) dec_k_pairs<D, IL, false>(qrow, s, kq, qraw[s][0], qraw[s][1]);
     }
   }
   const int ntiles = (nk + kDecWaveKeys - 1) / kDecWaveKeys;
@@ -1526,7 +1534,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int j0 = kDecWaveKeys * tile;
     const int r = nr == 1 ? 0 : min(j0 / rk, nr - 1);
     const int jr = j0 - r * rk + rgs[r].key_begin;
-    dec_fetch<D, IL>(cur, a.k_pool + rgs[r].k_offset + ((int64_t)g * rgs[r].k_stride + jr) * D,
+    dec_fetch<D, IL, false>(cur, a.k_pool + rgs[r].k_offset + ((int64_t)g * rgs[r].k_stride + jr) * D,
                      a.v_pool + rgs[r].v_offset + ((int64_t)g * rgs[r].v_stride + jr) * D,
                      min(kDecWaveKeys, nk - j0), lane);
   }
@@ -1595,7 +1603,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       const int j1 = kDecWaveKeys * next;
       int64_t k1, v1;
       run_key(srg, nr, rk, g, j1, D, k1, v1);
-      dec_fetch<D, IL>(nxt, a.k_pool + k1, a.v_pool + v1, min(kDecWaveKeys, nk - j1), lane);
+      dec_fetch<D, IL, false>(nxt, a.k_pool + k1, a.v_pool + v1, min(kDecWaveKeys, nk - j1), lane);
       if (ROT && lane < D / 2)
         *reinterpret_cast<float2*>(sm.csb[wave][buf ^ 1] + csb_idx<D>(lane)) = rope_cs(j1, sm.freq[lane]);
     }
@@ -1840,7 +1848,10 @@ hipError_t prefill_d(const AttnArgs& a, hipStream_t st) {
 template <int D, int KM>
 hipError_t decode_d(const AttnArgs& a, hipStream_t st) {
   const dim3 grid(a.splits, a.hkv * a.head_groups, a.batch);
-  hipLaunchKernelGGL((decode_kernel<D, KM>), grid, dim3(kThreads), 0, st, a);
+  if (a.stream_kv)
+    hipLaunchKernelGGL((decode_kernel<D, KM | kStreamKV>), grid, dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((decode_kernel<D, KM>), grid, dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 

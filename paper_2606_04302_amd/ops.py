@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblazyattn
 LAZY_OK, LAZY_EINVAL, LAZY_EUNSUPPORTED, LAZY_EWORKSPACE, LAZY_EHIP, LAZY_EDATA = 0, -1, -2, -3, -4, -5
 KEYS_NOPE, KEYS_LOCAL = 0, 1  # key-store conventions (lazy_attn_params_t.key_positions)
 ROPE_HALF, ROPE_INTERLEAVED, ALIBI = 0, 1, 2  # positional method (lazy_attn_params_t.rope_style)
+CACHE_DEFAULT, CACHE_STREAM = 0, 1  # K / V cache hint (lazy_attn_params_t.cache_hint)
 
 _c_i32, _c_i64, _c_f32, _c_p, _c_sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -36,6 +37,7 @@ class LazyAttnParams(ctypes.Structure):
         ("key_positions", _c_i32),
         ("rope_style", _c_i32),
         ("q_prerotated", _c_i32),
+        ("cache_hint", _c_i32),
     ]
 
 
@@ -140,12 +142,14 @@ class Config:
     key_positions: int = 0  # KEYS_NOPE or KEYS_LOCAL
     rope_style: int = 0  # ROPE_HALF, ROPE_INTERLEAVED or ALIBI (then inv_freq optionally holds the Hq slopes)
     q_prerotated: bool = False  # q already holds R(q_pos) q
+    cache_hint: int = 0  # CACHE_DEFAULT or CACHE_STREAM (decode: non-temporal K / V loads)
 
     def c(self) -> LazyAttnParams:
         return LazyAttnParams(self.num_q_heads, self.num_kv_heads, self.head_dim, int(bool(self.causal)),
                               float(self.rope_base), float(self.softmax_scale),
                               None if self.inv_freq is None else self.inv_freq.data_ptr(), int(self.num_splits),
-                              int(self.key_positions), int(self.rope_style), int(bool(self.q_prerotated)))
+                              int(self.key_positions), int(self.rope_style), int(bool(self.q_prerotated)),
+                              int(self.cache_hint))
 
 
 def config_of(w: Workload, **kw) -> Config:

@@ -56,7 +56,8 @@ def test_struct_layout_matches_header(tmp_path, ops):
         " offsetof(lazy_chunk_t, v_stride), sizeof(lazy_attn_params_t));"
         'printf("%zu %zu %zu %zu\\n", offsetof(lazy_attn_params_t, rope_base), offsetof(lazy_attn_params_t, inv_freq),'
         " offsetof(lazy_attn_params_t, num_splits), offsetof(lazy_attn_params_t, key_positions));"
-        'printf("%zu %zu\\n", offsetof(lazy_attn_params_t, rope_style), offsetof(lazy_attn_params_t, q_prerotated));'
+        'printf("%zu %zu %zu\\n", offsetof(lazy_attn_params_t, rope_style), offsetof(lazy_attn_params_t, q_prerotated),'
+        " offsetof(lazy_attn_params_t, cache_hint));"
         "return 0;}"
     )
     exe = tmp_path / "layout"
@@ -65,7 +66,7 @@ def test_struct_layout_matches_header(tmp_path, ops):
     c = [int(x) for x in a.split()]
     p = [int(x) for x in b.split()]
     LC, LP = ops.LazyChunk, ops.LazyAttnParams
-    assert [int(x) for x in e.split()] == [LP.rope_style.offset, LP.q_prerotated.offset]
+    assert [int(x) for x in e.split()] == [LP.rope_style.offset, LP.q_prerotated.offset, LP.cache_hint.offset]
     assert c == [ctypes.sizeof(LC), LC.v_offset.offset, LC.len.offset, LC.pos_offset.offset, LC.k_stride.offset,
                  LC.v_stride.offset, ctypes.sizeof(LP)]
     assert p == [LP.rope_base.offset, LP.inv_freq.offset, LP.num_splits.offset, LP.key_positions.offset]
@@ -153,6 +154,9 @@ def test_scalar_argument_errors_return_before_any_launch(ops):
     assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0, 0, 2)) == ops.LAZY_EINVAL   # q_prerotated is 0 or 1
     assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0, 0, -1)) == ops.LAZY_EINVAL
     assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0, 0, 1), batch=0) == ops.LAZY_OK
+    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0, 0, 0, 2)) == ops.LAZY_EINVAL  # cache hint is 0 or 1
+    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0, 0, 0, -1)) == ops.LAZY_EINVAL
+    assert prefill(P(8, 2, 128, 1, 1e4, 0.0, None, 0, 0, 0, 0, 1), batch=0) == ops.LAZY_OK
     assert prefill(good, batch=-1) == ops.LAZY_EINVAL
     assert prefill(good, batch=0) == ops.LAZY_OK                                       # nothing to do
     assert prefill(good, total_q=0) == ops.LAZY_OK

@@ -163,6 +163,46 @@ def test_decode_matches_oracle(name):
     run_and_check(W.rag_decode(**kw), "decode " + name, ckw)
 
 
+# Cache hint LAZY_CACHE_STREAM: the decode entry points read K and V with non-temporal loads.  Only the cache policy
+# of those loads changes, so every output must be bit-identical to the default hint's; the streamed NoPE result is
+# also checked against the oracle.
+STREAM_MODES = {"nope": {}, "local": dict(key_positions=ops.KEYS_LOCAL), "interleaved": dict(rope_style=ops.ROPE_INTERLEAVED),
+                "alibi": dict(rope_style=ops.ALIBI), "plain": {}, "noalloc": {}}
+
+
+@pytest.mark.parametrize("mode", list(STREAM_MODES))
+@pytest.mark.parametrize("name", ["d128_g4", "d128_g4_split1", "d64_g7_split5"])
+def test_stream_cache_hint_decode_is_bitwise_the_default(name, mode):
+    kw, ckw = DECODE_CASES[name]
+    w = W.rag_decode(**kw)
+    dw = ops.upload(w)
+    plain = None
+    if mode == "plain":
+        total = int(w.chunks["len"].astype(np.int64).sum())
+        plain = ops.materialize_k(dw.cfg, dw.pool, dw.chunks, int(w.chunks["len"].max()), total)
+    res = []
+    for hint in (ops.CACHE_DEFAULT, ops.CACHE_STREAM):
+        cfg = ops.config_of(w, **ckw, **STREAM_MODES[mode], cache_hint=hint)
+        if mode == "noalloc":
+            out = torch.empty_like(dw.q)
+            lse = torch.empty((w.total_q, w.num_q_heads), dtype=torch.float32, device="cuda")
+            ops.decode_noalloc(cfg, dw.q, dw.q_pos0, dw.pool, dw.pool, dw.chunks, dw.chunk_start,
+                               max(1, w.max_kv_len), out, lse)
+            torch.cuda.synchronize()
+            res.append((out.clone(), lse.clone()))
+        elif plain is not None:
+            res.append(ops.run_lazy(dw, cfg, plain_k=plain[0], plain_chunks=plain[1]))
+        else:
+            res.append(ops.run_lazy(dw, cfg))
+    torch.cuda.synchronize()
+    (o0, l0), (o1, l1) = res
+    assert torch.equal(o0.view(torch.int16), o1.view(torch.int16)), (name, mode)
+    assert torch.equal(l0, l1), (name, mode)
+    if mode == "nope":
+        ref_o, ref_l = oracle(w)
+        assert_close(o1, l1, ref_o, ref_l, tag=f"stream hint {name}")
+
+
 @pytest.mark.parametrize("kind", ["prefill", "decode"])
 def test_lazy_equals_materialize_then_attend_bitwise(kind):
     if kind == "prefill":
