@@ -115,9 +115,12 @@ typedef struct lazy_attn_params {
  *  LAZY_CACHE_DEFAULT (0): ordinary loads.  Right whenever the call's chunks are shared between its requests, or are
  *                          read again soon enough to still be in the last-level cache (a pool that fits in it).
  *  LAZY_CACHE_STREAM  (1): the decode entry points (lazy_attn_decode, lazy_plain_attn_decode,
- *                          lazy_attn_decode_noalloc) read K and V with non-temporal loads, which stream faster from
- *                          HBM but give up the cache reuse above: for requests whose contexts are private and larger
- *                          than the last-level cache, read once per decode step.  Other entry points ignore it.
+ *                          lazy_attn_decode_noalloc, lazy_attn_decode_shared) read K and V with non-temporal loads,
+ *                          which stream faster from HBM but give up the cache reuse above: for requests whose
+ *                          contexts are private and larger than the last-level cache, read once per decode step.  In
+ *                          the shared decode an item holds at most 16 / G users, so a chunk with more users is read
+ *                          by several workgroups: there too the hint only pays for private contexts.  Other entry
+ *                          points ignore it.
  * Any other value is LAZY_EINVAL.
  */
 #define LAZY_CACHE_DEFAULT 0

@@ -349,6 +349,7 @@ int lazy_attn_decode_shared(const lazy_attn_params_t* p, const void* q, const in
   a.interleaved = p->rope_style == LAZY_ROPE_INTERLEAVED;
   a.alibi = p->rope_style == LAZY_ALIBI;
   a.q_prerot = p->q_prerotated && p->rope_style != LAZY_ALIBI;
+  a.stream_kv = p->cache_hint == LAZY_CACHE_STREAM;
   a.rope_log2_base = p->inv_freq || p->rope_style == LAZY_ALIBI ? 0.0 : log2((double)p->rope_base);
   a.scale_log2 = scale_log2(p);
   return status(lazy::launch_decode_shared(a, num_items, max_slots, slot_start, p->head_dim,

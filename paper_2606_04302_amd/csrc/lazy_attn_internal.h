@@ -63,6 +63,7 @@ struct SharedArgs {
   int32_t interleaved;
   int32_t alibi;
   int32_t q_prerot;
+  int32_t stream_kv;                 // 1 reads K / V with non-temporal loads (LAZY_CACHE_STREAM)
   double rope_log2_base;
   float scale_log2;
 };

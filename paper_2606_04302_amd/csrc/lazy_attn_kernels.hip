@@ -1489,7 +1489,7 @@ template <int D, int KMI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_shared_kernel(
     SharedArgs a) {
   constexpr int KM = keys_of(KMI);
-  constexpr bool IL = interleaved_of(KMI), ALIBI = KM == kKeysAlibi;
+  constexpr bool IL = interleaved_of(KMI), ALIBI = KM == kKeysAlibi, NT = stream_of(KMI);
   __shared__ DecodeSmem<D> sm;
   __shared__ float ucs[16][DecodeSmem<D>::CSB];  // per user: cos/sin(rel theta_t) at csb_idx(t)
   using S = DecodeSmem<D>;
@@ -1534,7 +1534,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int j0 = kDecWaveKeys * tile;
     const int r = nr == 1 ? 0 : min(j0 / rk, nr - 1);
     const int jr = j0 - r * rk + rgs[r].key_begin;
-    dec_fetch<D, IL, false>(cur, a.k_pool + rgs[r].k_offset + ((int64_t)g * rgs[r].k_stride + jr) * D,
+    dec_fetch<D, IL, NT>(cur, a.k_pool + rgs[r].k_offset + ((int64_t)g * rgs[r].k_stride + jr) * D,
                      a.v_pool + rgs[r].v_offset + ((int64_t)g * rgs[r].v_stride + jr) * D,
                      min(kDecWaveKeys, nk - j0), lane);
   }
@@ -1603,7 +1603,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       const int j1 = kDecWaveKeys * next;
       int64_t k1, v1;
       run_key(srg, nr, rk, g, j1, D, k1, v1);
-      dec_fetch<D, IL, false>(nxt, a.k_pool + k1, a.v_pool + v1, min(kDecWaveKeys, nk - j1), lane);
+      dec_fetch<D, IL, NT>(nxt, a.k_pool + k1, a.v_pool + v1, min(kDecWaveKeys, nk - j1), lane);
       if (ROT && lane < D / 2)
         *reinterpret_cast<float2*>(sm.csb[wave][buf ^ 1] + csb_idx<D>(lane)) = rope_cs(j1, sm.freq[lane]);
     }
@@ -1884,19 +1884,30 @@ hipError_t decode_dk(const AttnArgs& a, int km, hipStream_t st) {
     default: return decode_d<D, kKeysLocal | kInterleaved>(a, st);
   }
 }
+template <int D, int NT>
+void shared_dk_nt(const SharedArgs& a, int km, dim3 grid, hipStream_t st) {
+  switch (km) {
+    case kKeysAlibi:
+      hipLaunchKernelGGL((decode_shared_kernel<D, kKeysAlibi | NT>), grid, dim3(kThreads), 0, st, a);
+      break;
+    case kKeysNope: hipLaunchKernelGGL((decode_shared_kernel<D, kKeysNope | NT>), grid, dim3(kThreads), 0, st, a); break;
+    case kKeysLocal:
+      hipLaunchKernelGGL((decode_shared_kernel<D, kKeysLocal | NT>), grid, dim3(kThreads), 0, st, a);
+      break;
+    case kKeysNope | kInterleaved:
+      hipLaunchKernelGGL((decode_shared_kernel<D, kKeysNope | kInterleaved | NT>), grid, dim3(kThreads), 0, st, a);
+      break;
+    default:
+      hipLaunchKernelGGL((decode_shared_kernel<D, kKeysLocal | kInterleaved | NT>), grid, dim3(kThreads), 0, st, a);
+  }
+}
 template <int D>
 void shared_dk(const SharedArgs& a, dim3 grid, hipStream_t st) {
   const int km = a.alibi ? kKeysAlibi : (a.local_keys ? kKeysLocal : kKeysNope) | (a.interleaved ? kInterleaved : 0);
-  switch (km) {
-    case kKeysAlibi: hipLaunchKernelGGL((decode_shared_kernel<D, kKeysAlibi>), grid, dim3(kThreads), 0, st, a); break;
-    case kKeysNope: hipLaunchKernelGGL((decode_shared_kernel<D, kKeysNope>), grid, dim3(kThreads), 0, st, a); break;
-    case kKeysLocal: hipLaunchKernelGGL((decode_shared_kernel<D, kKeysLocal>), grid, dim3(kThreads), 0, st, a); break;
-    case kKeysNope | kInterleaved:
-      hipLaunchKernelGGL((decode_shared_kernel<D, kKeysNope | kInterleaved>), grid, dim3(kThreads), 0, st, a);
-      break;
-    default:
-      hipLaunchKernelGGL((decode_shared_kernel<D, kKeysLocal | kInterleaved>), grid, dim3(kThreads), 0, st, a);
-  }
+  if (a.stream_kv)
+    shared_dk_nt<D, kStreamKV>(a, km, grid, st);
+  else
+    shared_dk_nt<D, 0>(a, km, grid, st);
 }
 template <int D>
 void materialize_dk(bool local, bool il, dim3 grid, hipStream_t st, const uint16_t* k_pool, const lazy_chunk_t* in,

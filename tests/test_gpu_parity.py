@@ -167,7 +167,8 @@ def test_decode_matches_oracle(name):
 # of those loads changes, so every output must be bit-identical to the default hint's; the streamed NoPE result is
 # also checked against the oracle.
 STREAM_MODES = {"nope": {}, "local": dict(key_positions=ops.KEYS_LOCAL), "interleaved": dict(rope_style=ops.ROPE_INTERLEAVED),
-                "alibi": dict(rope_style=ops.ALIBI), "plain": {}, "noalloc": {}}
+                "alibi": dict(rope_style=ops.ALIBI), "plain": {}, "noalloc": {}, "shared": {},
+                "shared_local": dict(key_positions=ops.KEYS_LOCAL)}
 
 
 @pytest.mark.parametrize("mode", list(STREAM_MODES))
@@ -190,6 +191,12 @@ def test_stream_cache_hint_decode_is_bitwise_the_default(name, mode):
                                max(1, w.max_kv_len), out, lse)
             torch.cuda.synchronize()
             res.append((out.clone(), lse.clone()))
+        elif mode.startswith("shared"):
+            lse = torch.empty((w.total_q, w.num_q_heads), dtype=torch.float32, device="cuda")
+            plan = ops.upload_plan(ops.shared_decode_plan(cfg, w.chunks, w.chunk_start, 256))
+            out, lse = ops.decode_shared(cfg, dw.q, dw.q_pos0, dw.pool, dw.pool, plan, lse=lse)
+            torch.cuda.synchronize()
+            res.append((out.clone(), lse.clone()))
         elif plain is not None:
             res.append(ops.run_lazy(dw, cfg, plain_k=plain[0], plain_chunks=plain[1]))
         else:
@@ -198,9 +205,9 @@ def test_stream_cache_hint_decode_is_bitwise_the_default(name, mode):
     (o0, l0), (o1, l1) = res
     assert torch.equal(o0.view(torch.int16), o1.view(torch.int16)), (name, mode)
     assert torch.equal(l0, l1), (name, mode)
-    if mode == "nope":
+    if mode in ("nope", "shared"):
         ref_o, ref_l = oracle(w)
-        assert_close(o1, l1, ref_o, ref_l, tag=f"stream hint {name}")
+        assert_close(o1, l1, ref_o, ref_l, tag=f"stream hint {mode} {name}")
 
 
 @pytest.mark.parametrize("kind", ["prefill", "decode"])
