@@ -1497,8 +1497,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   constexpr bool ROT = KM == kKeysNope;
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   __shared__ lazy_shared_range_t srg[LAZY_SHARED_MAX_RANGES];
-  const cptr<lazy_shared_item_t> item = as_const(a.items) + blockIdx.x;
-  const int g = blockIdx.y;
+  // Workgroup (item, KV head) = the logical id under the contiguous map of xcd_remap: XCD k takes the k-th eighth of
+  // the item-major ids (one KV head's items in plan order), so the items of one run (a chunk with more users than an
+  // item holds) run together on one XCD and read its keys through one L2.
+  const int lid = uniform(xcd_remap(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y, gridDim.x,
+                                    gridDim.y, false));
+  const cptr<lazy_shared_item_t> item = as_const(a.items) + lid % gridDim.x;
+  const int g = lid / gridDim.x;
   // Item fields come from the planner (lazy_shared_decode_validate checks a plan on the host).  The clamps keep
   // every LDS index in bounds whatever the item holds: the range table (at most LAZY_SHARED_MAX_RANGES entries) and
   // the per-user angle rows (at most floor(16 / G) users, one MFMA column per (user, query head)).
