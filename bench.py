@@ -234,6 +234,8 @@ def other_configs(dev, steps: int, warmup: int, log):
       request, 256-token causal query at 32,768), its prefill, then 128 decode steps (the query's own chunk grows
       by one token per step, one query per request at the newest position).  The baseline materialises the
       rotated keys once (at the final lengths, so the appended keys are included) and runs the plain kernels.
+      Timed twice: with the tables in position order, and (``storage_order``) with every request's table in
+      storage order, the baseline taking the same tables.
     - varlen_rag: 16 requests, 28/4 heads, D=128, base 1e6, 8-24 chunks of U[128, 2048] tokens per request drawn
       Zipf(2.1) without replacement from a 200-chunk pool, queries of U[32, 256] tokens."""
     import torch
@@ -352,9 +354,86 @@ def other_configs(dev, steps: int, warmup: int, log):
     plain_dec_ms = timed(lambda: decode_all(k_mat, plain_tabs), reps, 2)
     lazy_total = pre_ms + dec_ms
     base_total = mat_ms + plain_pre_ms + plain_dec_ms
+
+    # The same per-request prefill and decode steps with every request's table in storage order
+    # (lazy_chunk_table_storage_order; positions, not the table order, decide the attention).  The decode's
+    # workgroups for one (split, KV head) of the four requests run together on one XCD, so with the exemplars listed
+    # in the same order the requests read each one through one L2.  The baseline takes the same tables (its copy is
+    # written in that order and V is still read from the pool).
+    log("icl: storage-ordered tables")
+    so_tables = []
+    for ch, _, qp in tables:
+        t = ops.storage_order(ch, w.chunk_start)
+        so_tables.append((t, ops.chunks_tensor(t, dev), qp))
+    so_own = []
+    for r, i in enumerate(own):
+        a, b = int(w.chunk_start[r]), int(w.chunk_start[r + 1])
+        so_own.append(a + int(np.flatnonzero(so_tables[0][0]["k_offset"][a:b] == w.chunks[i]["k_offset"])[0]))
+    so_pre_np = so_tables[0][0].copy()
+    for r, i in enumerate(so_own):
+        so_pre_np[i]["len"] = int(w.q_lens[r])
+    so_pre_t = ops.chunks_tensor(so_pre_np, dev)
+
+    def so_prefill(c):
+        return lambda: ops.prefill(c, dw.q, dw.q_start, dw.q_pos0, dw.pool, dw.pool, so_pre_t, dw.chunk_start,
+                                   w.max_q_len, w.max_kv_len, out=out, workspace=ws)
+
+    def so_decode(c, kp=None, plain_tables=None):
+        def run():
+            for s, (_, ch, qp) in enumerate(so_tables):
+                if plain_tables is None:
+                    ops.decode(c, qd, qp, dw.pool, dw.pool, ch, dw.chunk_start, max_kv, out=outd, workspace=wsd)
+                else:
+                    ops.decode(c, qd, qp, kp, dw.pool, plain_tables[s], dw.chunk_start, max_kv, out=outd,
+                               workspace=wsd, plain=True)
+        return run
+
+    so_pre_ms = timed(so_prefill(cfg), steps, warmup)
+    so_dec_ms = timed(so_decode(cfg), reps, 2)
+    so_local_pre_ms = timed(so_prefill(cfg_local), steps, warmup)
+    so_local_dec_ms = timed(so_decode(cfg_local), reps, 2)
+    so_mat_fn, so_k_mat, so_ch_mat = materialized(w, dw, so_tables[-1][0])
+    so_mat_fn()
+    torch.cuda.synchronize()
+    so_mat_np = ops.chunks_from_tensor(so_ch_mat)
+    so_pre_tab = so_mat_np.copy()
+    for r, i in enumerate(so_own):
+        so_pre_tab[i]["len"] = int(w.q_lens[r])
+    so_pre_tab_t = ops.chunks_tensor(so_pre_tab, dev)
+    so_plain_tabs = []
+    for ch, _, _ in so_tables:
+        t = so_mat_np.copy()
+        for i in so_own:
+            t[i]["len"] = int(ch[i]["len"])
+        so_plain_tabs.append(ops.chunks_tensor(t, dev))
+    so_mat_ms = timed(so_mat_fn, max(5, steps // 5), 2)
+    so_plain_pre_ms = timed(lambda: ops.prefill(cfg, dw.q, dw.q_start, dw.q_pos0, so_k_mat, dw.pool, so_pre_tab_t,
+                                                dw.chunk_start, w.max_q_len, w.max_kv_len, out=out, workspace=ws,
+                                                plain=True), steps, warmup)
+    so_plain_dec_ms = timed(so_decode(cfg, so_k_mat, so_plain_tabs), reps, 2)
+    so_lazy_total = so_pre_ms + so_dec_ms
+    so_base_total = so_mat_ms + so_plain_pre_ms + so_plain_dec_ms
+    storage_order = {
+        "prefill_ms": round(so_pre_ms, 5),
+        "decode_128_steps_ms": round(so_dec_ms, 4),
+        "decode_logical_gbps": round(dec_bytes / (so_dec_ms * 1e-3) / 1e9, 1),
+        "local_keys_prefill_ms": round(so_local_pre_ms, 5),
+        "local_keys_decode_128_steps_ms": round(so_local_dec_ms, 4),
+        "materialize_ms": round(so_mat_ms, 5),
+        "plain_prefill_ms": round(so_plain_pre_ms, 5),
+        "plain_decode_128_steps_ms": round(so_plain_dec_ms, 4),
+        "lazy_prefill_plus_decode_ms": round(so_lazy_total, 4),
+        "materialize_then_attend_ms": round(so_base_total, 4),
+        "speedup_vs_materialize": round(so_base_total / so_lazy_total, 3),
+        "local_keys_speedup_vs_materialize": round(so_base_total / (so_local_pre_ms + so_local_dec_ms), 3),
+        "speedup_vs_position_ordered_materialize": round(base_total / so_lazy_total, 3),
+    }
+    del so_k_mat
     res["icl"] = {
         "workload": "icl: batch 4, 32/8 heads, head_dim 128, base 5e5, 128 x 256-token exemplars (shared pool, "
-                    "permuted per request), 256-token query at 32,768, then 128 decode steps",
+                    "permuted per request), 256-token query at 32,768, then 128 decode steps; tables in position "
+                    "order, and under storage_order the same runs with each request's table in storage order "
+                    "(lazy and baseline alike)",
         "prefill_ms": round(pre_ms, 5),
         "prefill_tflops": round(flops / (pre_ms * 1e-3) / 1e12, 3),
         "prefill_mfma_frac": round(flops / (pre_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 5),
@@ -377,6 +456,7 @@ def other_configs(dev, steps: int, warmup: int, log):
         "local_keys_prefill_ms": round(local_pre_ms, 5),
         "local_keys_decode_128_steps_ms": round(local_dec_ms, 4),
         "local_keys_speedup_vs_materialize": round(base_total / (local_pre_ms + local_dec_ms), 3),
+        "storage_order": storage_order,
     }
     del k_mat, dw, ws, wsd
 
@@ -753,10 +833,22 @@ def main() -> int:
                      max(5, args.steps // 5), 2)
         dplain = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, kmd, dd.pool, chd, dd.chunk_start, wd.max_kv_len,
                                           out=outd, lse=lsed, workspace=wsd, plain=True), args.steps, args.warmup)
+        # Every request's table in storage order (lazy_chunk_table_storage_order), for the lazy decode and the
+        # baseline alike: the 64 requests' workgroups of one KV head run on one XCD and read the chunks they share
+        # in the same order.
+        so_t = ops.chunks_tensor(ops.storage_order(wd.chunks, wd.chunk_start), dev)
+        dso = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, dd.pool, dd.pool, so_t, dd.chunk_start, wd.max_kv_len,
+                                       out=outd, lse=lsed, workspace=wsd), args.steps, args.warmup)
+        dso_mat = timed(lambda: ops.materialize_k(cfgd, dd.pool, so_t, mxc, tkv, k_out=kmd, chunks_out=chd),
+                        max(5, args.steps // 5), 2)
+        dso_plain = timed(lambda: ops.decode(cfgd, dd.q, dd.q_pos0, kmd, dd.pool, chd, dd.chunk_start,
+                                             wd.max_kv_len, out=outd, lse=lsed, workspace=wsd, plain=True),
+                          args.steps, args.warmup)
         gbps = dbytes / (dms * 1e-3) / 1e9
         result["decode"] = {
             "workload": "rag_decode: batch 64, 32/8 heads, head_dim 128, 16 x 1024-token chunks from a 256-chunk "
-                        "pool + 65-token private tail, one query per request",
+                        "pool + 65-token private tail, one query per request; tables in position order, and under "
+                        "storage_order in storage order (lazy and baseline alike)",
             "ms": round(dms, 5),
             "logical_hbm_gbps": round(gbps, 1),
             "hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
@@ -783,6 +875,11 @@ def main() -> int:
             "plain_decode_ms": round(dplain, 5),
             "materialize_then_attend_ms": round(dmat + dplain, 5),
             "speedup_vs_materialize": round((dmat + dplain) / dms, 3),
+            "storage_order": {"ms": round(dso, 5),
+                              "logical_hbm_gbps": round(dbytes / (dso * 1e-3) / 1e9, 1),
+                              "logical_hbm_frac": round(dbytes / (dso * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+                              "materialize_ms": round(dso_mat, 5), "plain_decode_ms": round(dso_plain, 5),
+                              "speedup_vs_materialize": round((dso_mat + dso_plain) / dso, 3)},
             "traffic": recorded_traffic("decode_kernel_rag_decode"),
         }
         del kmd, dd

@@ -175,3 +175,20 @@ extern "C" int lazy_shared_decode_plan(const lazy_attn_params_t* p, const lazy_c
   }
   return LAZY_OK;
 }
+
+// Chunk table in storage order: each request's records, stably sorted by k_offset.  The attention a request gets is
+// fixed by its records' positions, not by their order in the table, so only the traversal order changes.
+extern "C" int lazy_chunk_table_storage_order(const lazy_chunk_t* chunks, const int32_t* chunk_start, int32_t batch,
+                                              lazy_chunk_t* out) {
+  if (!chunk_start || batch < 0 || chunk_start[0] != 0) return LAZY_EINVAL;
+  for (int32_t r = 0; r < batch; ++r)
+    if (chunk_start[r + 1] < chunk_start[r]) return LAZY_EINVAL;
+  const int32_t n = chunk_start[batch];
+  if (n == 0) return LAZY_OK;
+  if (!chunks || !out) return LAZY_EINVAL;
+  if (out != chunks) std::copy(chunks, chunks + n, out);
+  for (int32_t r = 0; r < batch; ++r)
+    std::stable_sort(out + chunk_start[r], out + chunk_start[r + 1],
+                     [](const lazy_chunk_t& a, const lazy_chunk_t& b) { return a.k_offset < b.k_offset; });
+  return LAZY_OK;
+}

@@ -81,6 +81,7 @@ SIGNATURES = {
     "lazy_attn_decode_shared": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_p,
                                          _c_p, _c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_sz, _c_p]),
     "lazy_attn_decode_shared_workspace_size": (_c_sz, [ctypes.POINTER(LazyAttnParams), _c_i32, _c_i32]),
+    "lazy_chunk_table_storage_order": (_c_i32, [_c_p, _c_p, _c_i32, _c_p]),
     "lazy_shared_decode_validate": (_c_i32, [ctypes.POINTER(LazyAttnParams), _c_p, _c_i32, _c_p, _c_i32, _c_p,
                                              _c_i32, _c_p, _c_i32, _c_i32, _c_p, _c_i64, _c_i64,
                                              ctypes.POINTER(_c_i64), ctypes.POINTER(ctypes.c_char_p)]),
@@ -405,6 +406,17 @@ def shared_decode_plan(cfg: Config, chunks: np.ndarray, chunk_start, max_keys_pe
         return SharedPlan(items[: n_items.value].copy(), ranges[: n_ranges.value].copy(), users[: n_users.value].copy(),
                           slot_start)
     raise RuntimeError("lazy_shared_decode_plan: capacity did not converge")
+
+
+def storage_order(chunks: np.ndarray, chunk_start) -> np.ndarray:
+    """lazy_chunk_table_storage_order on host tables: a copy with each request's records sorted by k_offset."""
+    chunks = np.ascontiguousarray(chunks, dtype=CHUNK_DTYPE)
+    cs = np.ascontiguousarray(chunk_start, dtype=np.int32)
+    out = np.empty_like(chunks)
+    _check(lib().lazy_chunk_table_storage_order(chunks.ctypes.data if chunks.size else None, cs.ctypes.data,
+                                                cs.size - 1, out.ctypes.data if out.size else None),
+           "lazy_chunk_table_storage_order")
+    return out
 
 
 def validate_shared_plan(cfg: Config, plan: SharedPlan, q_pos, k_pool_elems: int, v_pool_elems: int,

@@ -611,3 +611,50 @@ def test_shared_plan_validator_slot_coverage_pools_and_args(ops):
     L = ops.lib()
     assert L.lazy_shared_decode_validate(None, None, 0, None, 0, None, 0, plan.slot_start.ctypes.data, 0, 0, None,
                                          0, 0, None, None) == ops.LAZY_EINVAL
+
+
+@pytest.mark.parametrize("make", ["icl", "rag_decode", "paged", "repeated"])
+def test_storage_order_is_a_stable_sort_per_request(ops, make):
+    if make == "icl":
+        w = W.icl_prefill(seed=7, batch=3, hq=4, hkv=2, d=64, n_chunks=9, chunk_len=40, q_len=5, decode_steps=2)
+    elif make == "rag_decode":
+        w = W.rag_decode(seed=8, batch=5, hq=8, hkv=2, n_chunks=4, chunk_len=100, pool_chunks=6, tail_len=3,
+                         tail_cap=8)
+    elif make == "paged":
+        w = W.paginate(W.rag_decode(seed=9, batch=3, hq=8, hkv=2, n_chunks=3, chunk_len=130, pool_chunks=4,
+                                    tail_len=5, tail_cap=8), 32, seed=2)
+    else:  # one request reading the same stored chunk twice, at two offsets (equal keys keep their order)
+        w = W.icl_prefill(seed=10, batch=2, hq=4, hkv=2, d=64, n_chunks=4, chunk_len=32, q_len=3, decode_steps=1)
+        ch = w.chunks.copy()
+        ch[2]["k_offset"], ch[2]["v_offset"] = ch[0]["k_offset"], ch[0]["v_offset"]
+        w.chunks[:] = ch
+    out = ops.storage_order(w.chunks, w.chunk_start)
+    for r in range(w.batch):
+        a, b = int(w.chunk_start[r]), int(w.chunk_start[r + 1])
+        src, got = w.chunks[a:b], out[a:b]
+        order = np.argsort(src["k_offset"], kind="stable")
+        assert np.array_equal(got.view(np.uint8), src[order].view(np.uint8)), r
+        assert np.all(np.diff(got["k_offset"]) >= 0)
+    # in place (out aliases the input) gives the same table
+    inplace = np.ascontiguousarray(w.chunks).copy()
+    cs = np.ascontiguousarray(w.chunk_start, dtype=np.int32)
+    L = ops.lib()
+    assert L.lazy_chunk_table_storage_order(inplace.ctypes.data, cs.ctypes.data, cs.size - 1,
+                                            inplace.ctypes.data) == ops.LAZY_OK
+    assert np.array_equal(inplace.view(np.uint8), out.view(np.uint8))
+
+
+def test_storage_order_errors(ops):
+    L = ops.lib()
+    ch = np.zeros(3, dtype=ops.CHUNK_DTYPE)
+    out = np.zeros_like(ch)
+    good = np.array([0, 1, 3], dtype=np.int32)
+    assert L.lazy_chunk_table_storage_order(ch.ctypes.data, good.ctypes.data, 2, out.ctypes.data) == ops.LAZY_OK
+    for bad in ([1, 1, 3], [0, 2, 1]):
+        cs = np.array(bad, dtype=np.int32)
+        assert L.lazy_chunk_table_storage_order(ch.ctypes.data, cs.ctypes.data, 2, out.ctypes.data) == ops.LAZY_EINVAL
+    assert L.lazy_chunk_table_storage_order(ch.ctypes.data, good.ctypes.data, -1, out.ctypes.data) == ops.LAZY_EINVAL
+    assert L.lazy_chunk_table_storage_order(None, good.ctypes.data, 2, out.ctypes.data) == ops.LAZY_EINVAL
+    assert L.lazy_chunk_table_storage_order(ch.ctypes.data, None, 2, out.ctypes.data) == ops.LAZY_EINVAL
+    empty = np.zeros(1, dtype=np.int32)
+    assert L.lazy_chunk_table_storage_order(None, empty.ctypes.data, 0, None) == ops.LAZY_OK

@@ -890,3 +890,25 @@ def test_eight_wave_prefill_short_splits(mode):
     assert w.max_q_len * (w.num_q_heads // w.num_kv_heads) >= 256  # the eight-wave kernel
     for splits in (1, 2, 3, 4, 6):
         run_and_check(w, f"eight-wave prefill {mode} splits={splits}", {**ckw, "num_splits": splits})
+
+
+# --------------------------------------------------------------------------------------------------------------
+# Chunk tables in storage order (lazy_chunk_table_storage_order): the same records, each request's sorted by
+# k_offset.  Positions decide the attention, so the results match the oracle of the position-ordered table, and the
+# lazy path still equals materialise-then-attend over the reordered table bit for bit.
+@pytest.mark.parametrize("kind,ckw", [("decode", {}), ("decode", dict(num_splits=3)),
+                                      ("decode", dict(key_positions=ops.KEYS_LOCAL)), ("prefill", {}),
+                                      ("prefill", dict(num_splits=2))])
+def test_storage_ordered_tables_match_oracle(kind, ckw):
+    w = W.icl_prefill(seed=171, batch=3, hq=8, hkv=2, d=128, n_chunks=6, chunk_len=96, q_len=40, decode_steps=4)
+    if kind == "decode":
+        w = W.icl_decode_step(w, 2, seed=172)
+    ws = dataclasses.replace(w, chunks=ops.storage_order(w.chunks, w.chunk_start))
+    assert not np.array_equal(ws.chunks.view(np.uint8), w.chunks.view(np.uint8))  # the order did change
+    dw, out, lse = run_and_check(ws, f"storage order {kind} {ckw}", ckw)
+    ref_o, ref_l = oracle(w, **oracle_kw(ckw))  # the position-ordered table
+    assert_close(out, lse, ref_o, ref_l, tag=f"storage order vs position-order oracle {kind} {ckw}")
+    if not ckw.get("key_positions"):
+        (out_m, lse_m), _ = ops.run_materialized(dw, ops.config_of(ws, **ckw))
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), out_m.view(torch.int16))
