@@ -315,15 +315,15 @@ LAZY_API int lazy_shared_decode_plan(const lazy_attn_params_t* params, const laz
 
 /*
  * Chunk table in storage order (host only, on HOST copies): out receives the records of chunks with each request's
- * records stably sorted by k_offset (out may be chunks itself).  A request's attention is set by its records'
- * positions, not by their order in the table (Sec. 3.2: chunks at any offsets), so a table in either order gives the
- * same result up to the order of the floating-point sums.  Why a caller would want it: the per-request kernels walk
- * a request's keys in table order, and the decode's workgroups for one (split, KV head) of all requests run at the
- * same time on one XCD when splits x ceil(G / 16) x Hkv is a multiple of 8 (always with 8 KV heads); requests whose
- * tables list the chunks they share in the same order then read those chunks together, through one L2, instead of
- * each from memory.  The chunk-major shared decode's planner wants tables in position order instead (it chains the
- * blocks a request reads back to back).  Returns LAZY_EINVAL for a bad chunk_start (not starting at 0, decreasing)
- * or missing arrays.
+ * records stably sorted by k_offset (out may be chunks itself; otherwise the two must not overlap).  A request's
+ * attention is set by its records' positions, not by their order in the table (Sec. 3.2: chunks at any offsets), so
+ * a table in either order gives the same result up to the order of the floating-point sums.  Why a caller would want
+ * it: the per-request kernels walk a request's keys in table order, and the decode's workgroups for one (split, KV
+ * head) of all requests are placed on one XCD when splits x ceil(G / 16) x Hkv is a multiple of 8 (always with 8 KV
+ * heads), all running at once when the grid fits the chip (two workgroups per CU); requests whose tables list the
+ * chunks they share in the same order then read those chunks together, through one L2, instead of each from memory.  The chunk-major shared decode's planner wants tables in
+ * position order instead (it chains the blocks a request reads back to back).  Returns LAZY_EINVAL for a bad
+ * chunk_start (not starting at 0, decreasing) or missing arrays.
  */
 LAZY_API int lazy_chunk_table_storage_order(const lazy_chunk_t* chunks, const int32_t* chunk_start, int32_t batch,
                                             lazy_chunk_t* out);
