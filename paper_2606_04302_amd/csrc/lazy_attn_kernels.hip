@@ -1492,6 +1492,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   constexpr bool IL = interleaved_of(KMI), ALIBI = KM == kKeysAlibi, NT = stream_of(KMI);
   __shared__ DecodeSmem<D> sm;
   __shared__ float ucs[16][DecodeSmem<D>::CSB];  // per user: cos/sin(rel theta_t) at csb_idx(t)
+  __shared__ int uang[16];                         // per user: (q_pos, or 0 for pre-rotated queries) - pos_offset
   using S = DecodeSmem<D>;
   constexpr int SP = DecTile<D>::SP;
   constexpr bool ROT = KM == kKeysNope;
@@ -1521,6 +1522,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int cuser = cvalid ? cu : 0;
   const lazy_shared_user_t usr = a.users[u0 + cuser];
   const int rel = a.q_pos[usr.request] - usr.pos_offset;
+  // The lane of each user's first column publishes its query angle offset, so that the per-user angle rows below
+  // need no second round of user and position loads.
+  if (wave == 0 && kq == 0 && cvalid && col % G == 0) uang[cu] = a.q_prerot ? -usr.pos_offset : rel;
 
   // Raw Q of this lane's column and the first tile's K / V before the tables (as in decode_kernel).
   u32x4 qraw[SP][2];
@@ -1559,9 +1563,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int qrot_shift = KM == kKeysLocal ? rgs[0].key_begin : 0;
   for (int e = tid; e < (ALIBI ? 0 : nu * (D / 2)); e += kThreads) {
     const int u = e / (D / 2), t = e % (D / 2);
-    const lazy_shared_user_t uu = a.users[u0 + u];
-    *reinterpret_cast<float2*>(&ucs[u][csb_idx<D>(t)]) =
-        rope_cs((a.q_prerot ? 0 : a.q_pos[uu.request]) - uu.pos_offset + qrot_shift, sm.freq[t]);
+    *reinterpret_cast<float2*>(&ucs[u][csb_idx<D>(t)]) = rope_cs(uang[u] + qrot_shift, sm.freq[t]);
   }
   __syncthreads();
 
