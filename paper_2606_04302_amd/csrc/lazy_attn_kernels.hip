@@ -1293,13 +1293,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   }
   if (!ALIBI && tid < D / 2) sm.freq[tid] = theta_rev(tid, D, a.rope_log2_base, a.inv_freq);
   __syncthreads();
-  if (ROT) {
-    // Per-row constants cos/sin(delta theta_t), delta < 32: 16 per thread.
-    for (int e = tid; e < kDecWaveKeys * (D / 2); e += kThreads) {
-      const int dr = e / (D / 2), t = e % (D / 2);
-      *reinterpret_cast<float2*>(sm.csd + dec_row<D>(dr) + 2 * t) = rope_cs(dr, sm.freq[t]);
-    }
-  }
   // This wave's tiles: every fourth tile of the split, starting at tile `wave`.
   TileIter<kDecWaveKeys> it;
   it.init(a.chunks, c0, c1, split, a.splits, first);
@@ -1309,6 +1302,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   if (have)
     dec_fetch<D, IL, NT>(cur, k_ptr(a.k_pool, it.cur, g, it.j0, D), v_ptr(a.v_pool, it.cur, g, it.j0, D),
                  min(kDecWaveKeys, it.cur.len - it.j0), lane);
+  if (ROT) {
+    // Per-row constants cos/sin(delta theta_t), delta < 32: 16 per thread, while the first tile is in flight.
+    for (int e = tid; e < kDecWaveKeys * (D / 2); e += kThreads) {
+      const int dr = e / (D / 2), t = e % (D / 2);
+      *reinterpret_cast<float2*>(sm.csd + dec_row<D>(dr) + 2 * t) = rope_cs(dr, sm.freq[t]);
+    }
+  }
   if (ROT && have && lane < D / 2)
     *reinterpret_cast<float2*>(sm.csb[wave][0] + csb_idx<D>(lane)) = rope_cs(it.cur.pos + it.j0, sm.freq[lane]);
 #pragma unroll
