@@ -898,11 +898,20 @@ def test_eight_wave_prefill_short_splits(mode):
 # lazy path still equals materialise-then-attend over the reordered table bit for bit.
 @pytest.mark.parametrize("kind,ckw", [("decode", {}), ("decode", dict(num_splits=3)),
                                       ("decode", dict(key_positions=ops.KEYS_LOCAL)), ("prefill", {}),
-                                      ("prefill", dict(num_splits=2))])
+                                      ("prefill", dict(num_splits=2)), ("paged_decode", dict(num_splits=2)),
+                                      ("g7_decode", dict(cache_hint=ops.CACHE_STREAM))])
 def test_storage_ordered_tables_match_oracle(kind, ckw):
-    w = W.icl_prefill(seed=171, batch=3, hq=8, hkv=2, d=128, n_chunks=6, chunk_len=96, q_len=40, decode_steps=4)
-    if kind == "decode":
-        w = W.icl_decode_step(w, 2, seed=172)
+    if kind == "paged_decode":  # 32-token blocks scattered over the pool: storage order interleaves chunks
+        w = W.paginate(W.rag_decode(seed=173, batch=3, hq=8, hkv=2, n_chunks=3, chunk_len=150, pool_chunks=4,
+                                    tail_len=5, tail_cap=8), 32, seed=3)
+    elif kind == "g7_decode":
+        w = W.rag_decode(seed=174, batch=4, hq=28, hkv=4, n_chunks=4, chunk_len=120, pool_chunks=6, tail_len=7,
+                         tail_cap=12)
+    else:
+        w = W.icl_prefill(seed=171, batch=3, hq=8, hkv=2, d=128, n_chunks=6, chunk_len=96, q_len=40,
+                          decode_steps=4)
+        if kind == "decode":
+            w = W.icl_decode_step(w, 2, seed=172)
     ws = dataclasses.replace(w, chunks=ops.storage_order(w.chunks, w.chunk_start))
     assert not np.array_equal(ws.chunks.view(np.uint8), w.chunks.view(np.uint8))  # the order did change
     dw, out, lse = run_and_check(ws, f"storage order {kind} {ckw}", ckw)
