@@ -405,12 +405,29 @@ FULL = {
 }
 
 
+def _storage_ordered(w):
+    return dataclasses.replace(w, chunks=ops.storage_order(w.chunks, w.chunk_start))
+
+
+# The benchmark's storage-order legs at full size: the same records, each request's table in storage order.
+FULL_STORAGE_ORDER = {
+    "icl_decode_step64": (lambda: _storage_ordered(W.icl_decode_step(W.icl_prefill(seed=3), 64)), list(range(4))),
+    "rag_decode": (lambda: _storage_ordered(W.rag_decode(seed=2)), [0, 37, 63]),
+}
+
+
 @pytest.mark.parametrize("name", list(FULL))
 def test_full_size_sampled(name):
     make, reqs = FULL[name]
     w = make()
     print(f"{name}: batch={w.batch} total_q={w.total_q} max_kv={w.max_kv_len} meta={w.meta}", flush=True)
     run_and_check(w, "full " + name, requests=reqs)
+
+
+@pytest.mark.parametrize("name", list(FULL_STORAGE_ORDER))
+def test_full_size_storage_order_sampled(name):
+    make, reqs = FULL_STORAGE_ORDER[name]
+    run_and_check(make(), "full storage order " + name, requests=reqs)
 
 
 # --------------------------------------------------------------------------------------------------------------
