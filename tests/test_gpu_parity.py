@@ -938,3 +938,18 @@ def test_storage_ordered_tables_match_oracle(kind, ckw):
         (out_m, lse_m), _ = ops.run_materialized(dw, ops.config_of(ws, **ckw))
         torch.cuda.synchronize()
         assert torch.equal(out.view(torch.int16), out_m.view(torch.int16))
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_shared_decode_on_storage_ordered_tables(paged):
+    """The shared decode's planner groups records by the stored keys they read, whatever the table order; on a paged
+    store in storage order the blocks of a chunk no longer follow each other in a request's table, so the planner
+    keeps them as separate items, and the results stay those of the position-ordered tables."""
+    w = W.rag_decode(seed=175, batch=5, hq=8, hkv=2, n_chunks=3, chunk_len=160, pool_chunks=4, tail_len=6, tail_cap=8)
+    if paged:
+        w = W.paginate(w, 32, seed=4)
+    ws = _storage_ordered(w)
+    plan = run_shared_and_check(ws, f"shared decode, storage order, paged={paged}")
+    base = ops.shared_decode_plan(ops.config_of(w), w.chunks, w.chunk_start)
+    assert plan.read_keys() == base.read_keys()  # every stored key still read once per step
+    assert plan.items.size == base.items.size if not paged else plan.items.size > base.items.size
